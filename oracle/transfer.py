@@ -1,0 +1,132 @@
+"""Transfer oracle: sender KV cache -> receiver KV cache, fp64 (test
+infrastructure; see package docstring).
+
+For one sequence, receiver layer l, role c in {K=0, V=1} and receiver token j:
+
+1. Layer interpolation (two nearest sender layers, weights from the integer
+   layer table):  m_i = a_lo * S[lo, c, :, i, :] + a_hi * S[hi, c, :, i, :]
+   (the hi tap is absent when rem == 0).
+2. Keys stored after the sender's RoPE are un-rotated at sender position
+   p_i = pos0_s + i with the sender's theta: u_i = U_s(p_i) m_i.  Values and
+   pre-RoPE keys pass unchanged.
+3. Token alignment: x_j = sum over the CSR row of (num / den_j) * u_i,
+   flattened head-major (feature index h * d_h + e) -- the flattened role-c
+   KV feature of Sec. 3.1 (Eq. 2 with one interpolated tap).
+4. Folded affine map of Eq. 9, written in column form: y_j = A[l, c] x_j
+   + b[l, c] with A stored [d_R, d_S] (the transpose of the paper's row-vector
+   A_final) and the scalar 1/r of Eq. 3 folded into A by the caller.
+5. Reshape into receiver KV heads and, for keys, apply the receiver's RoPE at
+   q_j = pos0_r + j with the receiver's theta (Sec. 3.3 "Folding for
+   inference"; App. B.1).
+6. R[l, c, h', j, e'] = y_j[h' * d_h + e'].
+
+Inputs are the exact stored values widened to fp64; the result stays fp64.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import scipy.sparse as sp
+
+from . import rope as _rope
+from .layer_map import interp2_weights
+
+K, V = 0, 1
+
+
+def _mix(S_lo, S_hi, a_lo, a_hi, rem):
+    m = a_lo * S_lo
+    if rem != 0:
+        m = m + a_hi * S_hi
+    return m
+
+
+def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None):
+    """Whole receiver cache of one sequence.
+
+    S           fp64-convertible [L_S, 2, H_S, T_S, d_h]
+    layer_table (lo, hi, rem, den) int arrays [L_R]
+    csr         (row_ptr[T_R+1], col, num, den[T_R]) for this sequence
+    A           [L_R, 2, d_R, d_S];  b  [L_R, 2, d_R] or None
+    rope        None or dict(theta_s, theta_r, unrotate_sender_k,
+                rotate_receiver_k, pos0_s, pos0_r)
+    returns     [L_R, 2, H_R, T_R, d_h] fp64
+    """
+    S = np.asarray(S, dtype=np.float64)
+    A = np.asarray(A, dtype=np.float64)
+    L_s, _, H_s, T_s, d_h = S.shape
+    L_r, _, d_r, d_in = A.shape
+    if d_in != H_s * d_h:
+        raise ValueError("A's input size must be H_S * d_h")
+    H_r = d_r // d_h if H_r is None else H_r
+    lo, hi, rem, den_l = (np.asarray(t) for t in layer_table)
+    a_lo, a_hi = interp2_weights(lo, hi, rem, den_l)
+    row_ptr, col, num, den = (np.asarray(t, dtype=np.int64) for t in csr)
+    T_r = row_ptr.size - 1
+    rows = np.repeat(np.arange(T_r), np.diff(row_ptr))
+    w = num.astype(np.float64) / den[rows].astype(np.float64)
+    W = sp.csr_matrix((w, col, row_ptr), shape=(T_r, T_s))
+    s_pos = r_pos = None
+    if rope is not None:
+        s_pos = rope.get("pos0_s", 0) + np.arange(T_s)
+        r_pos = rope.get("pos0_r", 0) + np.arange(T_r)
+    out = np.empty((L_r, 2, H_r, T_r, d_h), dtype=np.float64)
+    for l in range(L_r):
+        for c in (K, V):
+            m = _mix(S[lo[l], c], S[hi[l], c], a_lo[l], a_hi[l], rem[l])  # [H_s,T_s,d_h]
+            if c == K and rope is not None and rope.get("unrotate_sender_k", False):
+                m = _rope.unrotate(m, s_pos, rope["theta_s"])
+            u = m.transpose(1, 0, 2).reshape(T_s, H_s * d_h)               # head-major
+            x = W @ u                                                       # [T_r, d_S]
+            y = x @ A[l, c].T
+            if b is not None:
+                y = y + np.asarray(b, dtype=np.float64)[l, c][None, :]
+            y = y.reshape(T_r, H_r, d_h).transpose(1, 0, 2)                 # [H_r,T_r,d_h]
+            if c == K and rope is not None and rope.get("rotate_receiver_k", False):
+                y = _rope.rotate(y, r_pos, rope["theta_r"])
+            out[l, c] = y
+    return out
+
+
+def transfer_rows(get_sender, layer_table, csr, A_lc, b_lc, rope, d_h,
+                  layer, role, rows):
+    """Selected receiver rows of one (layer, role), entry by entry.
+
+    get_sender(l, c, idx) -> fp64 [H_S, len(idx), d_h] gives sender rows idx
+    of sender layer l, role c (only the rows the CSR entries name are asked
+    for).  A_lc is A[layer, role] ([d_R, d_S]); b_lc its bias or None.
+    Returns fp64 [H_R, len(rows), d_h].
+    """
+    lo, hi, rem, den_l = (np.asarray(t) for t in layer_table)
+    a_lo, a_hi = interp2_weights(lo, hi, rem, den_l)
+    row_ptr, col, num, den = (np.asarray(t, dtype=np.int64) for t in csr)
+    A_lc = np.asarray(A_lc, dtype=np.float64)
+    d_r, d_in = A_lc.shape
+    H_r = d_r // d_h
+    rows = np.asarray(rows, dtype=np.int64)
+    out = np.empty((H_r, rows.size, d_h), dtype=np.float64)
+    unrot = role == K and rope is not None and rope.get("unrotate_sender_k", False)
+    rot = role == K and rope is not None and rope.get("rotate_receiver_k", False)
+    for n, j in enumerate(rows):
+        ents = range(row_ptr[j], row_ptr[j + 1])
+        idx = np.asarray([col[e] for e in ents], dtype=np.int64)
+        S_lo = get_sender(int(lo[layer]), role, idx)
+        S_hi = get_sender(int(hi[layer]), role, idx) if rem[layer] != 0 else None
+        x = np.zeros(d_in, dtype=np.float64)
+        for q, e in enumerate(ents):
+            m = a_lo[layer] * S_lo[:, q, :]
+            if rem[layer] != 0:
+                m = m + a_hi[layer] * S_hi[:, q, :]
+            if unrot:
+                p = rope.get("pos0_s", 0) + int(col[e])
+                m = _rope.unrotate(m[:, None, :], [p], rope["theta_s"])[:, 0, :]
+            x += (float(num[e]) / float(den[j])) * m.reshape(-1)
+        y = A_lc @ x
+        if b_lc is not None:
+            y = y + np.asarray(b_lc, dtype=np.float64)
+        y = y.reshape(H_r, d_h)
+        if rot:
+            qpos = rope.get("pos0_r", 0) + int(j)
+            y = _rope.rotate(y[:, None, :], [qpos], rope["theta_r"])[:, 0, :]
+        out[:, n, :] = y
+    return out
