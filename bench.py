@@ -1,0 +1,201 @@
+"""Throughput of the HeteroFold transfer path on one MI355X.
+
+One step = one pass of the whole path over one synthetic batch:
+hf_build_alignment (GPU) -> hf_build_layer_map (host) -> hf_transfer_kv (GPU),
+with inputs already resident in HBM.  Prints ONE JSON line (rank 0):
+
+  value     receiver KV tokens per second (every receiver token of the batch,
+            all layers, K and V), whole step
+  roofline  the transfer kernel's achieved bf16 matrix-core TFLOP/s (algorithmic
+            flops per launch / mean launch time from HIP events recorded on the
+            launch stream over the timed steps) against the MI355X dense bf16 peak
+  cpu_baseline  the fp64 CPU oracle on a bounded sample of the same workload
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
+PEAK_HBM_GBS = 8000.0
+METRIC = "receiver KV tokens/sec (all layers, K+V) at 32K; % of MFMA/HBM roofline"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "transfer_bf16_14b_32k_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_32259_amd", "csrc", "transfer.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_cost(cfg, seg):
+    """Flops and HBM bytes of one transfer kernel launch:
+    flops = 2 roles x L_r x 2 d_in d_r per receiver token; bytes = each sender
+    layer the layer map uses read once per role, the receiver cache written
+    once, the maps read once."""
+    from paper_2609_32259_amd import heterofold as hf
+    T_r = int(seg.r_len.sum())
+    T_s = int(seg.s_len.sum())
+    el = 2 if cfg.dtype == "bf16" else 4
+    flops = 2 * cfg.L_r * 2 * cfg.d_in * cfg.d_r * T_r
+    lo, hi, rem, _ = hf.hf_build_layer_map(cfg.L_s, cfg.L_r)
+    used = set(lo.tolist()) | {int(h) for h, r in zip(hi, rem) if r}
+    read = len(used) * 2 * T_s * cfg.d_in * el
+    write = cfg.L_r * 2 * T_r * cfg.d_r * el
+    maps = cfg.L_r * 2 * cfg.d_r * cfg.d_in * el + cfg.L_r * 2 * cfg.d_r * 4
+    return flops, read + write + maps
+
+
+def kernel_traffic():
+    """HBM bytes per transfer launch from the committed rocprofv3 counter
+    summary, or None if there is none or the kernel source changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+        src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+        if rec.get("kernel_source_sha256") != src:
+            return None
+        return rec.get("bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def cpu_baseline(wl, budget_s=30.0):
+    """Time the fp64 oracle on the host: the full alignment of the batch plus
+    one receiver layer (K and V) at full length; scale to the whole step."""
+    from oracle import alignment as al
+    from oracle import layer_map as lm
+    from oracle import transfer as tr
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    cfg, seg = wl.cfg, wl.seg
+    t0 = time.perf_counter()
+    csr = [al.build_alignment(*seg.seq(b), "overlap") for b in range(seg.batch)]
+    t_align = time.perf_counter() - t0
+    lt = lm.interp2(cfg.L_s, cfg.L_r)
+    layer = 1 if cfg.L_r > 1 else 0
+    lo, hi = int(lt[0][layer]), int(lt[1][layer])
+    sub = (np.array([0]), np.array([1 if hi != lo else 0]), lt[2][layer:layer + 1], lt[3][layer:layer + 1])
+    t_layer = 0.0
+    for b in range(seg.batch):
+        T_s = int(seg.s_len[b])
+        taps = [lo] if hi == lo else [lo, hi]
+        S = wl.S[b, taps, :, :, :T_s, :].float().cpu().numpy().astype(np.float64)
+        A = wl.A[layer:layer + 1].float().cpu().numpy().astype(np.float64)
+        bias = wl.bias[layer:layer + 1].float().cpu().numpy().astype(np.float64)
+        rp = None if wl.rope is None else dict(wl.rope, pos0_s=0, pos0_r=0)
+        t0 = time.perf_counter()
+        tr.transfer(S, sub, csr[b], A, bias, rp, H_r=cfg.H_r)
+        t_layer += time.perf_counter() - t0
+        del S
+    est = t_align + cfg.L_r * t_layer
+    T_r = int(seg.r_len.sum())
+    return {"value": T_r / est, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle: full overlap alignment of the batch ({t_align:.2f} s) "
+                       f"+ receiver layer {layer} K and V at full length ({t_layer:.2f} s), "
+                       f"scaled to {cfg.L_r} layers: {est:.1f} s per step of {T_r} receiver tokens")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="14b-32k")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the transfer path is built and timed on a single "
+              f"MI355X; --gpus {args.gpus} is not supported (how it would shard is in DESIGN.md)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_32259_amd import heterofold as hf
+    from paper_2609_32259_amd import synth
+    from paper_2609_32259_amd.path import TransferPath
+
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    hf.lib()
+    cfg = synth.CONFIGS[args.workload]
+    log(f"[bench] workload {cfg.name}: generating inputs on the GPU")
+    wl = synth.make_workload(cfg, seed=args.seed, device="cuda")
+    path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r)
+    torch.cuda.synchronize()
+    T_r = int(wl.seg.r_len.sum())
+    T_s = int(wl.seg.s_len.sum())
+    log(f"[bench] B={wl.seg.batch} T_s={T_s} T_r={T_r}; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        path.step()
+    torch.cuda.synchronize()
+
+    hf.hf_profiler_reset()
+    hf.hf_profiler_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        path.step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    hf.hf_profiler_enable(False)
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    k_ms, k_n = hf.hf_profiler_query(hf.HF_KERNEL_TRANSFER)
+    a_ms, a_n = hf.hf_profiler_query(hf.HF_KERNEL_ALIGNMENT)
+    r_ms, r_n = hf.hf_profiler_query(hf.HF_KERNEL_ROPE_TABLES)
+    k_avg = k_ms / max(k_n, 1)
+    log(f"[bench] step {ms_step:.3f} ms; transfer kernel {k_avg:.3f} ms x{k_n}; "
+        f"alignment {a_ms / max(a_n, 1):.3f} ms; rope tables {r_ms / max(r_n, 1):.3f} ms")
+
+    flops, bytes_alg = algorithmic_cost(cfg, wl.seg)
+    achieved = flops / (k_avg * 1e-3) / 1e12
+    traffic = kernel_traffic()
+    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+            "kernel": "transfer_bf16_kernel", "kernel_ms": round(k_avg, 4),
+            "algorithmic_bytes": bytes_alg,
+            "hbm_GBps_algorithmic": round(bytes_alg / (k_avg * 1e-3) / 1e9, 1)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline(wl)
+    out = {
+        "metric": METRIC,
+        "value": round(T_r / (ms_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": wl.seg.batch, "T_s": T_s, "T_r": T_r,
+                   "L_s": cfg.L_s, "L_r": cfg.L_r, "H_s": cfg.H_s, "H_r": cfg.H_r, "d_h": cfg.d_h,
+                   "rope": list(cfg.rope) if cfg.rope else None, "alignment": "overlap",
+                   "layer_map": "interp2", "parallelism": "single-gpu"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,267 @@
+/*
+ * heterofold.h -- C ABI of the HeteroFold transfer-time path on AMD MI355X
+ * (gfx950).
+ *
+ * The path turns a frozen sender model's KV cache into a frozen receiver
+ * model's KV cache without running the receiver's prefill (Sec. 3, opening
+ * paragraph: map C_S(x) to a receiver-compatible cache).  It has four steps:
+ *
+ *   1. hf_build_alignment  -- which sender tokens each receiver token reads,
+ *      from the two tokenizers' character spans (Sec. 3.1 "Token Alignment";
+ *      App. B.1), as a CSR span table.
+ *   2. hf_build_layer_map  -- which sender layers feed each receiver layer.
+ *   3. hf_transfer_kv      -- gather, segment-mean and layer-interpolate the
+ *      sender cache, un-rotate post-RoPE sender keys, apply the folded affine
+ *      map y = A x + b of each receiver layer and role (Eq. 9), rotate keys at
+ *      the receiver's positions, and write the receiver cache.
+ *   4. (RoPE un-rotation / re-rotation is fused into step 3.)
+ *
+ * hf_pack_maps re-lays the static maps out once for the matrix-core kernel.
+ *
+ * Conventions for every call:
+ *  - Returns HF_OK (0) or a negative hf_status; hf_last_error() then holds a
+ *    thread-local description.  Nothing aborts and no C++ exception crosses
+ *    the ABI.
+ *  - "device" pointers are HIP device memory owned by the caller; "host"
+ *    pointers are host memory owned by the caller and read only during the
+ *    call.  The library allocates no device memory; scratch space comes from a
+ *    caller workspace whose size a *_workspace_bytes query gives.
+ *  - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *    runs asynchronously; no call synchronizes the host (the profiler query
+ *    excepted).  Launch errors are reported as HF_ERR_HIP.
+ *  - All host-checkable arguments are validated before anything is launched.
+ *    Device-side data that cannot be checked on the host (character offsets,
+ *    CSR contents) never causes an out-of-bounds access: indices are clamped
+ *    into the buffers the sizes describe.
+ *  - Character spans: token t of a sequence covers characters [beg[t], end[t]).
+ *    Valid spans are sorted and non-overlapping: 0 <= beg[t] <= end[t] <=
+ *    beg[t+1].  Empty tokens (beg == end) and gaps are allowed.  Results for
+ *    spans that break this rule are unspecified but memory-safe.
+ */
+#ifndef HETEROFOLD_H
+#define HETEROFOLD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HF_VERSION 1
+#define HF_MAX_BATCH 64   /* sequences per call */
+#define HF_MAX_LAYERS 128 /* receiver layers per call */
+
+typedef enum {
+  HF_OK = 0,
+  HF_ERR_NULL = -1,        /* a required pointer is NULL */
+  HF_ERR_SHAPE = -2,       /* sizes, strides or counts are inconsistent */
+  HF_ERR_OFFSETS = -3,     /* character spans break the sorted/non-overlapping rule (host check) */
+  HF_ERR_MODE = -4,        /* unknown alignment or layer mode */
+  HF_ERR_DTYPE = -5,       /* unknown or mismatched storage type */
+  HF_ERR_CAPACITY = -6,    /* an output or workspace buffer is too small */
+  HF_ERR_HIP = -7,         /* a HIP runtime call or kernel launch failed */
+  HF_ERR_UNSUPPORTED = -8  /* a valid shape this build has no kernel for */
+} hf_status;
+
+typedef enum { HF_ALIGN_OVERLAP = 0, HF_ALIGN_TA = 1 } hf_align_mode;
+typedef enum { HF_LAYERS_INTERP2 = 0 } hf_layer_mode;
+typedef enum { HF_F32 = 0, HF_BF16 = 1 } hf_dtype;
+
+/* Thread-local text of the last failure of a call made on this thread. */
+const char* hf_last_error(void);
+int32_t hf_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Step 1: cross-tokenizer alignment (Sec. 3.1 "Token Alignment"; App. B.1). */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Upper bound on the CSR entries hf_build_alignment writes for valid spans:
+ * sum over sequences of (T_s + 2 T_r).  s_cu, r_cu: host [B+1] prefix sums
+ * of the per-sequence sender / receiver token counts (s_cu[0] = r_cu[0] = 0).
+ * Returns -1 on bad arguments.
+ */
+int64_t hf_alignment_nnz_capacity(int32_t B, const int32_t* s_cu, const int32_t* r_cu);
+
+/* Workspace bytes hf_build_alignment needs for this batch. */
+size_t hf_alignment_workspace_bytes(int32_t B, const int32_t* r_cu);
+
+/*
+ * Build the alignment table of B independent sequences.
+ *
+ * Inputs
+ *   s_cu, r_cu        host int32 [B+1]: prefix sums of token counts.  A
+ *                     sequence with T_r > 0 needs T_s > 0.
+ *   s_beg, s_end      device int32 [s_cu[B]]: sender spans, sequences back to back.
+ *   r_beg, r_end      device int32 [r_cu[B]]: receiver spans.
+ *   mode              HF_ALIGN_TA: the paper's Token Alignment.  Nonempty
+ *                     sender and receiver tokens that end at the same character
+ *                     are paired (the largest such sender index); other
+ *                     receiver tokens take the sender token of the latest
+ *                     preceding shared boundary, or the first nonempty sender
+ *                     token before any (index 0 if none is nonempty).  One
+ *                     entry per row, weight 1.
+ *                     HF_ALIGN_OVERLAP: receiver token j reads every sender
+ *                     token i whose span overlaps its own, with weight
+ *                     num/den_j where num = shared characters and den_j = their
+ *                     sum; a row with no overlap holds its TA entry (weight 1).
+ * Outputs (device, caller-allocated)
+ *   row_ptr  int32 [r_cu[B]+1]  global CSR row offsets; row r_cu[b]+j is
+ *                               receiver token j of sequence b.
+ *   col      int32 [nnz_capacity]  sender token index, local to the sequence.
+ *   num      int32 [nnz_capacity]  weight numerator (1 in TA mode).
+ *   den      int32 [r_cu[B]]       weight denominator of the row.
+ *   Entries of a row are in ascending col order.  For valid spans the table
+ *   is unique and the result is bit-exact.
+ * nnz_capacity must be >= hf_alignment_nnz_capacity(); otherwise
+ * HF_ERR_CAPACITY.  (Spans that break the validity rule may need more; the
+ * kernels then drop entries past the capacity and clamp row_ptr to it.)
+ * workspace: device, >= hf_alignment_workspace_bytes() bytes, 16-B aligned.
+ */
+int32_t hf_build_alignment(int32_t B, const int32_t* s_cu, const int32_t* r_cu,
+                           const int32_t* s_beg, const int32_t* s_end,
+                           const int32_t* r_beg, const int32_t* r_end, int32_t mode,
+                           int32_t* row_ptr, int32_t* col, int32_t* num, int32_t* den,
+                           int64_t nnz_capacity, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* Host check of one sequence's spans against the validity rule above:
+ * HF_OK or HF_ERR_OFFSETS (HF_ERR_NULL / HF_ERR_SHAPE for bad arguments). */
+int32_t hf_validate_offsets_host(int32_t T, const int32_t* beg, const int32_t* end);
+
+/* ------------------------------------------------------------------------ */
+/* Step 2: layer map.                                                        */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * HF_LAYERS_INTERP2: receiver layer j (0-based) sits at sender depth
+ * p = j (L_s-1)/(L_r-1) and linearly interpolates sender layers lo = floor(p)
+ * and hi = min(lo+1, L_s-1) with weights (den-rem)/den and rem/den, where
+ * rem/den = p - lo exactly (rem == 0: a single tap).  L_r == 1 gives
+ * (0, 0, 0, 1).  Outputs are host int32 [L_r] each.  Pure host code.
+ * (The paper's own map feeds three sender layers at offsets -4, 0, +4 around
+ * a proportional depth, Eq. 1; this interpolating map is the two-tap variant.)
+ */
+int32_t hf_build_layer_map(int32_t L_s, int32_t L_r, int32_t mode, int32_t* lo, int32_t* hi,
+                           int32_t* rem, int32_t* den);
+
+/* ------------------------------------------------------------------------ */
+/* Step 3: KV transfer.                                                      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * A KV cache in device memory.  Element (b, l, c, h, t, e) -- sequence b,
+ * layer l, role c (0 = K, 1 = V), KV head h, token t, channel e -- lives at
+ * ptr + b*stride_b + l*stride_l + c*stride_c + h*stride_h + t*stride_t + e
+ * (strides in elements; channels contiguous).  The canonical layout
+ * [B][L][2][H][T_cap][d_h] is the receiver cache layout [L,2,H_kv,T,d_h] per
+ * sequence.  ptr and every stride must keep rows 16-byte aligned.
+ */
+typedef struct hf_kv_desc {
+  void* ptr;
+  int32_t dtype; /* hf_dtype */
+  int32_t L, H, d_h, T_cap;
+  int64_t stride_b, stride_l, stride_c, stride_h, stride_t;
+} hf_kv_desc;
+
+/*
+ * Rotary position embedding (rotate-half: channel k pairs with k + d_h/2,
+ * angle pos * theta^(-2k/d_h)).  Sender token i sits at pos0_s[b] + i and
+ * receiver token j at pos0_r[b] + j (host int32 [B], NULL = 0).  If
+ * unrotate_sender_k, the stored sender keys are post-RoPE and are un-rotated
+ * at sender positions with theta_s before mapping; if rotate_receiver_k the
+ * mapped keys are rotated at receiver positions with theta_r (the receiver
+ * applies its own RoPE to mapped keys: Sec. 3.3 "Folding for inference";
+ * App. B.1).  Angles are formed in fp64; the rotation runs in fp32.
+ */
+typedef struct hf_rope {
+  double theta_s, theta_r;
+  int32_t unrotate_sender_k, rotate_receiver_k;
+  const int32_t* pos0_s;
+  const int32_t* pos0_r;
+} hf_rope;
+
+/* Bytes of the packed maps for L_r receiver layers, 2 roles, d_r x d_in. */
+size_t hf_packed_maps_bytes(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype);
+
+/*
+ * Re-lay the folded maps out for hf_transfer_kv.  A: device [L_r][2][d_r][d_in]
+ * row-major in `dtype` (row n maps the flattened sender feature, head-major
+ * index h*d_h + e, to receiver feature n = h'*d_h + e'; this is the transpose
+ * of the paper's row-vector A_final of Eq. 9, with the scalar 1/r of Eq. 3
+ * already folded in).  A_packed: device, hf_packed_maps_bytes() bytes,
+ * 16-B aligned, not overlapping A.  Maps are static, so this runs once per
+ * model pair.  bf16 needs d_in % 16 == 0 and d_r % 32 == 0.
+ */
+int32_t hf_pack_maps(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype, const void* A,
+                     void* A_packed, void* stream);
+
+/* Workspace bytes hf_transfer_kv needs (RoPE cos/sin tables); 0 without RoPE. */
+size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                                   const hf_kv_desc* sender, const hf_kv_desc* receiver,
+                                   const hf_rope* rope);
+
+/*
+ * Map the sender caches of B sequences to receiver caches.  For receiver
+ * layer l, role c and receiver token j of sequence b:
+ *   m_i = a_lo S[lo_l, c, :, i, :] + a_hi S[hi_l, c, :, i, :]      (layer map)
+ *   u_i = U_s(pos0_s + i) m_i  for keys when rope->unrotate_sender_k, else m_i
+ *   x_j = sum over row j of (num/den_j) u_i, flattened head-major   (alignment)
+ *   y_j = A[l, c] x_j + bias[l, c]                                  (Eq. 9)
+ *   keys: y_j <- R_r(pos0_r + j) y_j per receiver head when rotate_receiver_k
+ *   R[l, c, h', j, e'] = y_j[h'*d_h + e']
+ * Arguments
+ *   s_len, r_len   host int32 [B]: token counts (<= sender/receiver T_cap).
+ *   row_ptr, col, num, den   device: the table hf_build_alignment wrote for
+ *                  the same batch (row r_cu[b]+j as documented there).
+ *   lo, hi, rem, den_l       host int32 [receiver->L]: hf_build_layer_map's table.
+ *   sender, receiver         cache descriptors; same dtype and d_h.
+ *                  receiver->L is L_r; d_in = sender->H*d_h, d_r = receiver->H*d_h.
+ *   A_packed       device: maps packed by hf_pack_maps (same L_r, d_r, d_in, dtype).
+ *   bias           device fp32 [L_r][2][d_r], or NULL for zero bias.
+ *   rope           NULL = no RoPE.
+ *   workspace      device, >= hf_transfer_workspace_bytes(), 256-B aligned.
+ * Numerics: HF_F32 computes in fp32 throughout.  HF_BF16 forms x_j in fp32,
+ * rounds it once to bf16 (round-to-nearest-even), multiplies on the matrix
+ * cores with fp32 accumulation, adds bias and rotates in fp32, and rounds the
+ * result once to bf16.
+ * Supported by this build: d_h == 128 for HF_BF16 with receiver H in
+ * {2, 4, 8}; any even d_h and H for HF_F32 (d_in <= 4096).  Other valid
+ * shapes return HF_ERR_UNSUPPORTED.  Receiver rows past r_len are not written.
+ */
+int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                       const int32_t* row_ptr, const int32_t* col, const int32_t* num,
+                       const int32_t* den, const int32_t* lo, const int32_t* hi,
+                       const int32_t* rem, const int32_t* den_l, const hf_kv_desc* sender,
+                       const hf_kv_desc* receiver, const void* A_packed, const float* bias,
+                       const hf_rope* rope, void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Kernel timing (tracing).                                                  */
+/* ------------------------------------------------------------------------ */
+
+typedef enum {
+  HF_KERNEL_TRANSFER = 0,   /* the main transfer kernel of hf_transfer_kv */
+  HF_KERNEL_ROPE_TABLES = 1,/* cos/sin table kernel of hf_transfer_kv */
+  HF_KERNEL_ALIGNMENT = 2,  /* the three kernels of hf_build_alignment, together */
+  HF_KERNEL_PACK = 3,       /* hf_pack_maps */
+  HF_KERNEL_COUNT = 4
+} hf_kernel_id;
+
+/*
+ * While enabled (on != 0), every launch of the kernels above is bracketed by
+ * a pair of HIP events recorded on its own stream.  hf_profiler_query waits
+ * for the recorded events and returns the summed duration in milliseconds and
+ * the number of launches since the last reset.  Host-thread safe.
+ */
+int32_t hf_profiler_enable(int32_t on);
+int32_t hf_profiler_reset(void);
+int32_t hf_profiler_query(int32_t kernel_id, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HETEROFOLD_H */

@@ -1,0 +1,503 @@
+// C ABI of the transfer path: argument validation, dispatch to the kernel
+// launchers, error reporting and the kernel-timing profiler.  Nothing here
+// touches the HIP runtime before all host-side checks of a call have passed,
+// and loading the library initializes nothing.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "heterofold.h"
+#include "hf_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int32_t fail(int32_t status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return status;
+}
+
+int32_t ok() {
+  g_err.clear();
+  return HF_OK;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---------------------------------------------------------------------------
+// Profiler: HIP event pairs around kernel launches, per kernel id.
+// ---------------------------------------------------------------------------
+struct EventPair {
+  int kernel;
+  hipEvent_t start, stop;
+};
+
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<EventPair> pending;
+  double total_ms[HF_KERNEL_COUNT] = {};
+  int64_t launches[HF_KERNEL_COUNT] = {};
+};
+
+Profiler& prof() {
+  static Profiler p;
+  return p;
+}
+
+// Scope that records a start event before and a stop event after the launches
+// made while it lives, when the profiler is on.
+class TimedLaunch {
+ public:
+  TimedLaunch(int kernel, hipStream_t s) : kernel_(kernel), s_(s) {
+    Profiler& p = prof();
+    std::lock_guard<std::mutex> g(p.mu);
+    if (!p.on) return;
+    if (hipEventCreate(&ev_.start) != hipSuccess) return;
+    if (hipEventCreate(&ev_.stop) != hipSuccess) {
+      (void)hipEventDestroy(ev_.start);
+      return;
+    }
+    if (hipEventRecord(ev_.start, s_) != hipSuccess) {
+      (void)hipEventDestroy(ev_.start);
+      (void)hipEventDestroy(ev_.stop);
+      return;
+    }
+    active_ = true;
+  }
+  ~TimedLaunch() {
+    if (!active_) return;
+    Profiler& p = prof();
+    std::lock_guard<std::mutex> g(p.mu);
+    if (hipEventRecord(ev_.stop, s_) != hipSuccess) {
+      (void)hipEventDestroy(ev_.start);
+      (void)hipEventDestroy(ev_.stop);
+      return;
+    }
+    ev_.kernel = kernel_;
+    p.pending.push_back(ev_);
+  }
+
+ private:
+  int kernel_;
+  hipStream_t s_;
+  EventPair ev_{};
+  bool active_ = false;
+};
+
+// Collect finished event pairs into the totals (waits for them).
+int32_t drain_profiler(Profiler& p) {
+  for (EventPair& e : p.pending) {
+    float ms = 0.f;
+    hipError_t st = hipEventSynchronize(e.stop);
+    if (st == hipSuccess) st = hipEventElapsedTime(&ms, e.start, e.stop);
+    (void)hipEventDestroy(e.start);
+    (void)hipEventDestroy(e.stop);
+    if (st != hipSuccess) {
+      p.pending.clear();
+      return fail(HF_ERR_HIP, "profiler event: %s", hipGetErrorString(st));
+    }
+    p.total_ms[e.kernel] += ms;
+    p.launches[e.kernel] += 1;
+  }
+  p.pending.clear();
+  return HF_OK;
+}
+
+int32_t hip_fail(hipError_t e, const char* what) {
+  return fail(HF_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Per-sequence counts from [B+1] prefix sums.
+int32_t check_prefix(const char* name, int32_t B, const int32_t* cu) {
+  if (cu[0] != 0) return fail(HF_ERR_SHAPE, "%s[0] must be 0", name);
+  for (int b = 0; b < B; ++b)
+    if (cu[b + 1] < cu[b]) return fail(HF_ERR_SHAPE, "%s is not non-decreasing at %d", name, b);
+  return HF_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int32_t check_desc(const char* name, const hf_kv_desc* d) {
+  if (!d) return fail(HF_ERR_NULL, "%s descriptor is NULL", name);
+  if (!d->ptr) return fail(HF_ERR_NULL, "%s->ptr is NULL", name);
+  if (d->dtype != HF_F32 && d->dtype != HF_BF16) return fail(HF_ERR_DTYPE, "%s->dtype %d unknown", name, d->dtype);
+  if (d->L < 1 || d->H < 1 || d->d_h < 2 || (d->d_h & 1) || d->T_cap < 0)
+    return fail(HF_ERR_SHAPE, "%s: need L>=1, H>=1, even d_h>=2, T_cap>=0", name);
+  const int64_t vec = d->dtype == HF_BF16 ? 8 : 4;  // elements per 16 bytes
+  if (!aligned16(d->ptr)) return fail(HF_ERR_SHAPE, "%s->ptr is not 16-byte aligned", name);
+  const int64_t st[5] = {d->stride_b, d->stride_l, d->stride_c, d->stride_h, d->stride_t};
+  for (int i = 0; i < 5; ++i)
+    if (st[i] < 0 || st[i] % vec) return fail(HF_ERR_SHAPE, "%s: strides must be >= 0 and keep rows 16-byte aligned", name);
+  if (d->d_h % vec) return fail(HF_ERR_SHAPE, "%s: d_h must be a multiple of %lld", name, (long long)vec);
+  if (d->stride_t < d->d_h) return fail(HF_ERR_SHAPE, "%s: stride_t < d_h", name);
+  return HF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* hf_last_error(void) { return g_err.c_str(); }
+
+int32_t hf_version(void) { return HF_VERSION; }
+
+int32_t hf_validate_offsets_host(int32_t T, const int32_t* beg, const int32_t* end) {
+  if (T < 0) return fail(HF_ERR_SHAPE, "T must be >= 0");
+  if (T > 0 && (!beg || !end)) return fail(HF_ERR_NULL, "beg/end is NULL");
+  for (int32_t t = 0; t < T; ++t) {
+    if (beg[t] < 0 || beg[t] > end[t])
+      return fail(HF_ERR_OFFSETS, "token %d: need 0 <= beg <= end (got %d, %d)", t, beg[t], end[t]);
+    if (t + 1 < T && end[t] > beg[t + 1])
+      return fail(HF_ERR_OFFSETS, "tokens %d and %d overlap or are out of order", t, t + 1);
+  }
+  return ok();
+}
+
+int64_t hf_alignment_nnz_capacity(int32_t B, const int32_t* s_cu, const int32_t* r_cu) {
+  if (B < 1 || B > HF_MAX_BATCH || !s_cu || !r_cu) {
+    fail(HF_ERR_SHAPE, "need 1 <= B <= %d and non-NULL prefix sums", HF_MAX_BATCH);
+    return -1;
+  }
+  if (check_prefix("s_cu", B, s_cu) || check_prefix("r_cu", B, r_cu)) return -1;
+  ok();
+  return (int64_t)s_cu[B] + 2 * (int64_t)r_cu[B];
+}
+
+size_t hf_alignment_workspace_bytes(int32_t B, const int32_t* r_cu) {
+  if (B < 1 || B > HF_MAX_BATCH || !r_cu) return 0;
+  int nblk = 0;
+  for (int b = 0; b < B; ++b) nblk += (r_cu[b + 1] - r_cu[b] + hf::kAlignBlock - 1) / hf::kAlignBlock;
+  return hf::align_workspace_bytes(nblk);
+}
+
+int32_t hf_build_alignment(int32_t B, const int32_t* s_cu, const int32_t* r_cu,
+                           const int32_t* s_beg, const int32_t* s_end, const int32_t* r_beg,
+                           const int32_t* r_end, int32_t mode, int32_t* row_ptr, int32_t* col,
+                           int32_t* num, int32_t* den, int64_t nnz_capacity, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  if (B < 1 || B > HF_MAX_BATCH) return fail(HF_ERR_SHAPE, "B=%d outside [1, %d]", B, HF_MAX_BATCH);
+  if (!s_cu || !r_cu) return fail(HF_ERR_NULL, "s_cu / r_cu is NULL");
+  if (mode != HF_ALIGN_OVERLAP && mode != HF_ALIGN_TA) return fail(HF_ERR_MODE, "alignment mode %d unknown", mode);
+  int32_t st;
+  if ((st = check_prefix("s_cu", B, s_cu)) || (st = check_prefix("r_cu", B, r_cu))) return st;
+  const int64_t nS = s_cu[B], nR = r_cu[B];
+  for (int b = 0; b < B; ++b)
+    if (r_cu[b + 1] > r_cu[b] && s_cu[b + 1] == s_cu[b])
+      return fail(HF_ERR_SHAPE, "sequence %d has receiver tokens but no sender tokens", b);
+  if (!row_ptr) return fail(HF_ERR_NULL, "row_ptr is NULL");
+  if (nR > 0 && (!r_beg || !r_end || !den)) return fail(HF_ERR_NULL, "receiver spans / den is NULL");
+  if (nS > 0 && (!s_beg || !s_end)) return fail(HF_ERR_NULL, "sender spans are NULL");
+  if (nR > 0 && (!col || !num)) return fail(HF_ERR_NULL, "col / num is NULL");
+  const int64_t need = nS + 2 * nR;
+  if (need > INT32_MAX) return fail(HF_ERR_SHAPE, "batch too large for int32 CSR offsets");
+  if (nnz_capacity < need)
+    return fail(HF_ERR_CAPACITY, "nnz_capacity %lld < required %lld", (long long)nnz_capacity, (long long)need);
+
+  hf::AlignArgs a;
+  std::memset(&a, 0, sizeof a);
+  int nblk = 0;
+  for (int b = 0; b < B; ++b) {
+    a.blk_start[b] = nblk;
+    a.s0[b] = s_cu[b];
+    a.Ts[b] = s_cu[b + 1] - s_cu[b];
+    a.r0[b] = r_cu[b];
+    a.Tr[b] = r_cu[b + 1] - r_cu[b];
+    nblk += (a.Tr[b] + hf::kAlignBlock - 1) / hf::kAlignBlock;
+  }
+  a.blk_start[B] = nblk;
+  const size_t ws_need = hf::align_workspace_bytes(nblk);
+  if (!workspace) return fail(HF_ERR_NULL, "workspace is NULL");
+  if (workspace_bytes < ws_need)
+    return fail(HF_ERR_CAPACITY, "workspace %zu bytes < required %zu", workspace_bytes, ws_need);
+  if (!aligned16(workspace)) return fail(HF_ERR_SHAPE, "workspace is not 16-byte aligned");
+  const size_t n = (size_t)(nblk > 0 ? nblk : 1);
+  char* w = static_cast<char*>(workspace);
+  a.blk_sum = reinterpret_cast<long long*>(w);
+  w += align_up(n * sizeof(long long), 256);
+  a.blk_off = reinterpret_cast<long long*>(w);
+  w += align_up(n * sizeof(long long), 256);
+  a.blk_last = reinterpret_cast<int32_t*>(w);
+  w += align_up(n * sizeof(int32_t), 256);
+  a.blk_carry = reinterpret_cast<int32_t*>(w);
+  a.s_beg = s_beg;
+  a.s_end = s_end;
+  a.r_beg = r_beg;
+  a.r_end = r_end;
+  a.row_ptr = row_ptr;
+  a.col = col;
+  a.num = num;
+  a.den = den;
+  a.cap = nnz_capacity;
+  a.mode = mode;
+  a.B = B;
+  a.nblk = nblk;
+  a.total_rows = (int32_t)nR;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    TimedLaunch t(HF_KERNEL_ALIGNMENT, s);
+    e = hf::launch_alignment(a, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "alignment launch");
+  return ok();
+}
+
+int32_t hf_build_layer_map(int32_t L_s, int32_t L_r, int32_t mode, int32_t* lo, int32_t* hi,
+                           int32_t* rem, int32_t* den) {
+  if (mode != HF_LAYERS_INTERP2) return fail(HF_ERR_MODE, "layer mode %d unknown", mode);
+  if (L_s < 1 || L_r < 1) return fail(HF_ERR_SHAPE, "layer counts must be >= 1");
+  if (!lo || !hi || !rem || !den) return fail(HF_ERR_NULL, "output table is NULL");
+  for (int32_t j = 0; j < L_r; ++j) {
+    if (L_r == 1) {
+      lo[j] = hi[j] = rem[j] = 0;
+      den[j] = 1;
+      continue;
+    }
+    const int64_t n = (int64_t)j * (L_s - 1), d = L_r - 1;
+    lo[j] = (int32_t)(n / d);
+    rem[j] = (int32_t)(n % d);
+    den[j] = (int32_t)d;
+    hi[j] = std::min(lo[j] + 1, L_s - 1);
+  }
+  return ok();
+}
+
+size_t hf_packed_maps_bytes(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype) {
+  if (L_r < 1 || d_r < 1 || d_in < 1) return 0;
+  const size_t el = dtype == HF_BF16 ? 2 : (dtype == HF_F32 ? 4 : 0);
+  return (size_t)L_r * 2 * (size_t)d_r * (size_t)d_in * el;
+}
+
+int32_t hf_pack_maps(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype, const void* A,
+                     void* A_packed, void* stream) {
+  if (dtype != HF_F32 && dtype != HF_BF16) return fail(HF_ERR_DTYPE, "dtype %d unknown", dtype);
+  if (L_r < 1 || L_r > HF_MAX_LAYERS || d_r < 1 || d_in < 1)
+    return fail(HF_ERR_SHAPE, "need 1 <= L_r <= %d, d_r >= 1, d_in >= 1", HF_MAX_LAYERS);
+  if (dtype == HF_BF16 && (d_in % 16 || d_r % 32))
+    return fail(HF_ERR_SHAPE, "bf16 maps need d_in %% 16 == 0 and d_r %% 32 == 0");
+  if (dtype == HF_F32 && (d_in % 4))
+    return fail(HF_ERR_SHAPE, "fp32 maps need d_in %% 4 == 0");
+  if (!A || !A_packed) return fail(HF_ERR_NULL, "A / A_packed is NULL");
+  if (!aligned16(A) || !aligned16(A_packed)) return fail(HF_ERR_SHAPE, "A / A_packed not 16-byte aligned");
+  const size_t bytes = hf_packed_maps_bytes(L_r, d_r, d_in, dtype);
+  const char* a0 = static_cast<const char*>(A);
+  const char* p0 = static_cast<const char*>(A_packed);
+  if (a0 < p0 + bytes && p0 < a0 + bytes) return fail(HF_ERR_SHAPE, "A and A_packed overlap");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    TimedLaunch t(HF_KERNEL_PACK, s);
+    e = hf::launch_pack_maps(dtype, 2 * L_r, d_r, d_in, A, A_packed, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "pack launch");
+  return ok();
+}
+
+namespace {
+
+struct RopeSizes {
+  int P_s = 0, P_r = 0;  // table rows (0 = table not needed)
+};
+
+int32_t rope_sizes(int32_t B, const int32_t* s_len, const int32_t* r_len, const hf_rope* rope,
+                   RopeSizes& rs) {
+  rs = RopeSizes();
+  if (!rope) return HF_OK;
+  for (int b = 0; b < B; ++b) {
+    const int64_t ps = rope->pos0_s ? rope->pos0_s[b] : 0;
+    const int64_t pr = rope->pos0_r ? rope->pos0_r[b] : 0;
+    if (ps < 0 || pr < 0) return fail(HF_ERR_SHAPE, "RoPE start positions must be >= 0");
+    if (ps + s_len[b] > INT32_MAX || pr + r_len[b] > INT32_MAX)
+      return fail(HF_ERR_SHAPE, "RoPE positions overflow int32");
+    if (rope->unrotate_sender_k) rs.P_s = std::max(rs.P_s, (int)(ps + s_len[b]));
+    if (rope->rotate_receiver_k) rs.P_r = std::max(rs.P_r, (int)(pr + r_len[b]));
+  }
+  return HF_OK;
+}
+
+size_t rope_bytes(int P, int d_h) { return align_up((size_t)P * (d_h / 2) * sizeof(float2), 256); }
+
+}  // namespace
+
+size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                                   const hf_kv_desc* sender, const hf_kv_desc* receiver,
+                                   const hf_rope* rope) {
+  if (B < 1 || B > HF_MAX_BATCH || !s_len || !r_len || !sender || !receiver) return 0;
+  RopeSizes rs;
+  if (rope_sizes(B, s_len, r_len, rope, rs) != HF_OK) return 0;
+  return rope_bytes(rs.P_s, sender->d_h) + rope_bytes(rs.P_r, receiver->d_h);
+}
+
+int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                       const int32_t* row_ptr, const int32_t* col, const int32_t* num,
+                       const int32_t* den, const int32_t* lo, const int32_t* hi,
+                       const int32_t* rem, const int32_t* den_l, const hf_kv_desc* sender,
+                       const hf_kv_desc* receiver, const void* A_packed, const float* bias,
+                       const hf_rope* rope, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  if (B < 1 || B > HF_MAX_BATCH) return fail(HF_ERR_SHAPE, "B=%d outside [1, %d]", B, HF_MAX_BATCH);
+  if (!s_len || !r_len) return fail(HF_ERR_NULL, "s_len / r_len is NULL");
+  if (!lo || !hi || !rem || !den_l) return fail(HF_ERR_NULL, "layer table is NULL");
+  if (!row_ptr || !col || !num || !den) return fail(HF_ERR_NULL, "alignment table is NULL");
+  if (!A_packed) return fail(HF_ERR_NULL, "A_packed is NULL");
+  int32_t st;
+  if ((st = check_desc("sender", sender)) || (st = check_desc("receiver", receiver))) return st;
+  if (sender->dtype != receiver->dtype) return fail(HF_ERR_DTYPE, "sender and receiver dtypes differ");
+  if (sender->d_h != receiver->d_h) return fail(HF_ERR_SHAPE, "sender and receiver d_h differ");
+  const int dtype = sender->dtype, d_h = sender->d_h;
+  const int L_s = sender->L, L_r = receiver->L;
+  if (L_r > HF_MAX_LAYERS) return fail(HF_ERR_SHAPE, "receiver layers %d > %d", L_r, HF_MAX_LAYERS);
+  if (L_s > 256) return fail(HF_ERR_SHAPE, "sender layers %d > 256", L_s);
+  if (!aligned16(A_packed)) return fail(HF_ERR_SHAPE, "A_packed not 16-byte aligned");
+  if (bias && (reinterpret_cast<uintptr_t>(bias) & 15u)) return fail(HF_ERR_SHAPE, "bias not 16-byte aligned");
+  const int d_in = sender->H * d_h;
+  if (dtype == HF_BF16) {
+    if (d_h != 128) return fail(HF_ERR_UNSUPPORTED, "bf16 path needs d_h == 128 (got %d)", d_h);
+    const int H = receiver->H;
+    if (H != 2 && H != 4 && H != 8)
+      return fail(HF_ERR_UNSUPPORTED, "bf16 path needs receiver H in {2,4,8} (got %d)", H);
+  } else if (d_in > 4096 || d_in % 4) {
+    return fail(HF_ERR_UNSUPPORTED, "fp32 path needs d_in <= 4096 and d_in %% 4 == 0");
+  }
+  int64_t sum_r = 0;
+  for (int b = 0; b < B; ++b) {
+    if (s_len[b] < 0 || r_len[b] < 0) return fail(HF_ERR_SHAPE, "negative length in sequence %d", b);
+    if (s_len[b] > sender->T_cap || r_len[b] > receiver->T_cap)
+      return fail(HF_ERR_SHAPE, "sequence %d longer than the cache capacity", b);
+    if (r_len[b] > 0 && s_len[b] == 0)
+      return fail(HF_ERR_SHAPE, "sequence %d has receiver tokens but no sender tokens", b);
+    sum_r += r_len[b];
+  }
+  if (sum_r > INT32_MAX) return fail(HF_ERR_SHAPE, "too many receiver tokens");
+  for (int j = 0; j < L_r; ++j) {
+    if (lo[j] < 0 || lo[j] >= L_s || hi[j] < 0 || hi[j] >= L_s)
+      return fail(HF_ERR_SHAPE, "layer table row %d names a sender layer outside [0, %d)", j, L_s);
+    if (den_l[j] < 1 || rem[j] < 0 || rem[j] >= den_l[j])
+      return fail(HF_ERR_SHAPE, "layer table row %d needs 0 <= rem < den", j);
+  }
+  if (rope && (!(rope->theta_s > 0) || !(rope->theta_r > 0) || !std::isfinite(rope->theta_s) ||
+               !std::isfinite(rope->theta_r)))
+    return fail(HF_ERR_SHAPE, "RoPE thetas must be finite and > 0");
+  RopeSizes rs;
+  if ((st = rope_sizes(B, s_len, r_len, rope, rs))) return st;
+  const size_t ws_need = rope_bytes(rs.P_s, d_h) + rope_bytes(rs.P_r, d_h);
+  if (ws_need > 0) {
+    if (!workspace) return fail(HF_ERR_NULL, "workspace is NULL");
+    if (workspace_bytes < ws_need)
+      return fail(HF_ERR_CAPACITY, "workspace %zu bytes < required %zu", workspace_bytes, ws_need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+      return fail(HF_ERR_SHAPE, "workspace is not 256-byte aligned");
+  }
+
+  hf::TransferArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.S = sender->ptr;
+  a.R = receiver->ptr;
+  a.Wp = A_packed;
+  a.bias = bias;
+  a.row_ptr = row_ptr;
+  a.col = col;
+  a.num = num;
+  a.den = den;
+  a.s_sb = sender->stride_b; a.s_sl = sender->stride_l; a.s_sc = sender->stride_c;
+  a.s_sh = sender->stride_h; a.s_st = sender->stride_t;
+  a.r_sb = receiver->stride_b; a.r_sl = receiver->stride_l; a.r_sc = receiver->stride_c;
+  a.r_sh = receiver->stride_h; a.r_st = receiver->stride_t;
+  a.L_r = L_r;
+  a.H_s = sender->H;
+  a.H_r = receiver->H;
+  a.d_h = d_h;
+  a.B = B;
+  a.rows_per_tile = hf::transfer_rows_per_tile(dtype, receiver->H, d_in);
+  int tiles = 0, row0 = 0;
+  for (int b = 0; b < B; ++b) {
+    a.tile_start[b] = tiles;
+    tiles += (r_len[b] + a.rows_per_tile - 1) / a.rows_per_tile;
+    a.Ts[b] = s_len[b];
+    a.Tr[b] = r_len[b];
+    a.row0[b] = row0;
+    row0 += r_len[b];
+    a.pos0_s[b] = rope && rope->pos0_s ? rope->pos0_s[b] : 0;
+    a.pos0_r[b] = rope && rope->pos0_r ? rope->pos0_r[b] : 0;
+  }
+  a.tile_start[B] = tiles;
+  a.tiles_per_lc = tiles;
+  if ((int64_t)tiles * L_r * 2 > INT32_MAX) return fail(HF_ERR_SHAPE, "too many work items");
+  for (int j = 0; j < L_r; ++j) {
+    a.lo[j] = (uint8_t)lo[j];
+    a.hi[j] = (uint8_t)hi[j];
+    a.wlo[j] = (float)((double)(den_l[j] - rem[j]) / (double)den_l[j]);
+    a.whi[j] = (float)((double)rem[j] / (double)den_l[j]);
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(workspace);
+  if (rope && rope->unrotate_sender_k && rs.P_s > 0) {
+    a.cs_s = reinterpret_cast<const float2*>(w);
+    a.unrot = 1;
+  }
+  if (rope && rope->rotate_receiver_k && rs.P_r > 0) {
+    a.cs_r = reinterpret_cast<const float2*>(w + rope_bytes(rs.P_s, d_h));
+    a.rot = 1;
+  }
+  if (tiles == 0) return ok();
+  hipError_t e = hipSuccess;
+  if (a.unrot || a.rot) {
+    TimedLaunch t(HF_KERNEL_ROPE_TABLES, s);
+    if (a.unrot) e = hf::launch_rope_table(const_cast<float2*>(a.cs_s), rs.P_s, d_h, rope->theta_s, s);
+    if (e == hipSuccess && a.rot)
+      e = hf::launch_rope_table(const_cast<float2*>(a.cs_r), rs.P_r, d_h, rope->theta_r, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "RoPE table launch");
+  {
+    TimedLaunch t(HF_KERNEL_TRANSFER, s);
+    e = hf::launch_transfer(dtype, a, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "transfer launch");
+  return ok();
+}
+
+int32_t hf_profiler_enable(int32_t on) {
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  p.on = on != 0;
+  return ok();
+}
+
+int32_t hf_profiler_reset(void) {
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  int32_t st = drain_profiler(p);
+  for (int k = 0; k < HF_KERNEL_COUNT; ++k) {
+    p.total_ms[k] = 0.0;
+    p.launches[k] = 0;
+  }
+  return st == HF_OK ? ok() : st;
+}
+
+int32_t hf_profiler_query(int32_t kernel_id, double* total_ms, int64_t* launches) {
+  if (kernel_id < 0 || kernel_id >= HF_KERNEL_COUNT) return fail(HF_ERR_SHAPE, "kernel id %d unknown", kernel_id);
+  if (!total_ms || !launches) return fail(HF_ERR_NULL, "output pointer is NULL");
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  int32_t st = drain_profiler(p);
+  if (st != HF_OK) return st;
+  *total_ms = p.total_ms[kernel_id];
+  *launches = p.launches[kernel_id];
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,82 @@
+// Internal interface between the C-ABI layer (abi.cpp) and the kernel files.
+// Plain structs passed by value as kernel arguments (kept under 4 KB).
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "heterofold.h"
+
+namespace hf {
+
+constexpr int kAlignBlock = 256;  // receiver rows per alignment workgroup
+
+struct AlignArgs {
+  const int32_t* s_beg;
+  const int32_t* s_end;
+  const int32_t* r_beg;
+  const int32_t* r_end;
+  int32_t* row_ptr;
+  int32_t* col;
+  int32_t* num;
+  int32_t* den;
+  long long* blk_sum;   // [nblk] entries counted by each workgroup
+  long long* blk_off;   // [nblk] exclusive prefix of blk_sum
+  int32_t* blk_last;    // [nblk] last TA partner found in the workgroup, -1 if none
+  int32_t* blk_carry;   // [nblk] TA partner carried into the workgroup
+  long long cap;        // entries the col/num buffers hold
+  int32_t mode;
+  int32_t B;
+  int32_t nblk;
+  int32_t total_rows;
+  int32_t blk_start[HF_MAX_BATCH + 1];  // first workgroup of each sequence
+  int32_t s0[HF_MAX_BATCH];             // first sender span of each sequence
+  int32_t Ts[HF_MAX_BATCH];
+  int32_t r0[HF_MAX_BATCH];             // first receiver span / CSR row of each sequence
+  int32_t Tr[HF_MAX_BATCH];
+};
+
+// Workspace layout of the alignment: four arrays of nblk entries.
+size_t align_workspace_bytes(int nblk);
+
+struct TransferArgs {
+  const void* S;        // sender cache
+  void* R;              // receiver cache
+  const void* Wp;       // packed maps
+  const float* bias;    // [L_r][2][d_r] or nullptr
+  const int32_t* row_ptr;
+  const int32_t* col;
+  const int32_t* num;
+  const int32_t* den;
+  const float2* cs_s;   // sender cos/sin table [P_s][d_h/2] or nullptr
+  const float2* cs_r;   // receiver cos/sin table [P_r][d_h/2] or nullptr
+  long long s_sb, s_sl, s_sc, s_sh, s_st;
+  long long r_sb, r_sl, r_sc, r_sh, r_st;
+  int32_t L_r, H_s, H_r, d_h;
+  int32_t unrot, rot;       // RoPE on keys: un-rotate sender / rotate receiver
+  int32_t B;
+  int32_t rows_per_tile;
+  int32_t tiles_per_lc;     // row tiles of one (layer, role), summed over the batch
+  int32_t tile_start[HF_MAX_BATCH + 1];
+  int32_t Ts[HF_MAX_BATCH];
+  int32_t Tr[HF_MAX_BATCH];
+  int32_t row0[HF_MAX_BATCH];    // first CSR row of each sequence
+  int32_t pos0_s[HF_MAX_BATCH];
+  int32_t pos0_r[HF_MAX_BATCH];
+  uint8_t lo[HF_MAX_LAYERS];
+  uint8_t hi[HF_MAX_LAYERS];
+  float wlo[HF_MAX_LAYERS];
+  float whi[HF_MAX_LAYERS];
+};
+
+// Rows per workgroup tile of the transfer kernels.
+int transfer_rows_per_tile(int dtype, int H_r, int d_in);
+
+hipError_t launch_alignment(const AlignArgs& a, hipStream_t s);
+hipError_t launch_rope_table(float2* tab, int P, int d_h, double theta, hipStream_t s);
+hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* A, void* Wp,
+                            hipStream_t s);
+hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s);
+
+}  // namespace hf

@@ -1,0 +1,167 @@
+"""C-ABI checks that need no GPU: the library loads and exports every
+declared symbol, host-only entry points, and host-side argument validation
+(every call below fails before touching the HIP runtime)."""
+
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import layer_map as lm
+from paper_2609_32259_amd import heterofold as hf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(hf.LIB_PATH):
+        from paper_2609_32259_amd import build
+        build.build()
+    return hf.lib()
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "heterofold.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hf_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    decl = _declared()
+    assert len(decl) >= 14
+    for name in decl:
+        assert hasattr(L, name), name
+    assert sorted(hf.exported_symbols()) == decl
+
+
+def test_version(L):
+    assert hf.hf_version() == 1
+
+
+@pytest.mark.parametrize("L_s,L_r", [(4, 6), (32, 40), (32, 28), (28, 32), (1, 3), (5, 1), (7, 7)])
+def test_layer_map_matches_oracle(L, L_s, L_r):
+    got = hf.hf_build_layer_map(L_s, L_r)
+    exp = lm.interp2(L_s, L_r)
+    for g, e in zip(got, exp):
+        assert np.array_equal(g, e)
+
+
+def test_layer_map_errors(L):
+    with pytest.raises(hf.HeteroFoldError) as ei:
+        hf.hf_build_layer_map(0, 3)
+    assert ei.value.status == -2
+    with pytest.raises(hf.HeteroFoldError) as ei:
+        hf.hf_build_layer_map(3, 3, mode=7)
+    assert ei.value.status == -4
+
+
+def test_validate_offsets_host(L):
+    hf.hf_validate_offsets_host([0, 3, 3, 5], [3, 3, 5, 9])
+    hf.hf_validate_offsets_host([], [])
+    for beg, end in (([0, 2], [3, 5]), ([2], [1]), ([-1], [0]), ([3, 0], [4, 1])):
+        with pytest.raises(hf.HeteroFoldError) as ei:
+            hf.hf_validate_offsets_host(beg, end)
+        assert ei.value.status == -3
+
+
+def test_nnz_capacity(L):
+    assert hf.hf_alignment_nnz_capacity([0, 10, 25], [0, 8, 20]) == 25 + 40
+    with pytest.raises(hf.HeteroFoldError):
+        hf.hf_alignment_nnz_capacity([1, 10], [0, 8])
+
+
+def _p(a):
+    return a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+def test_alignment_host_validation(L):
+    s_cu = np.array([0, 10], np.int32)
+    r_cu = np.array([0, 9], np.int32)
+    fake = C.c_void_p(0x1000)
+    args = lambda **kw: dict(dict(B=1, s_cu=_p(s_cu), r_cu=_p(r_cu), sb=fake, se=fake, rb=fake, re=fake,  # noqa: E731
+                                  mode=0, rp=fake, col=fake, num=fake, den=fake, cap=28, ws=fake,
+                                  wsb=1 << 20, st=None), **kw)
+
+    def call(a):
+        return L.hf_build_alignment(a["B"], a["s_cu"], a["r_cu"], a["sb"], a["se"], a["rb"],
+                                    a["re"], a["mode"], a["rp"], a["col"], a["num"], a["den"],
+                                    a["cap"], a["ws"], a["wsb"], a["st"])
+
+    assert call(args(B=0)) == -2
+    assert call(args(mode=5)) == -4
+    assert call(args(rp=None)) == -1
+    assert call(args(col=None)) == -1
+    assert call(args(cap=27)) == -6
+    assert call(args(ws=None)) == -1
+    assert call(args(wsb=1)) == -6
+    bad = np.array([0, 0], np.int32)
+    assert call(args(s_cu=_p(bad))) == -2   # receiver tokens but no sender tokens
+    assert L.hf_last_error().decode()
+
+
+def _desc(ptr=0x1000, dtype=1, L_=4, H=8, d=128, T=64):
+    st_t = d
+    st_h = T * d
+    st_c = H * st_h
+    st_l = 2 * st_c
+    st_b = L_ * st_l
+    return hf.hf_kv_desc(C.c_void_p(ptr), dtype, L_, H, d, T, st_b, st_l, st_c, st_h, st_t)
+
+
+def test_transfer_host_validation(L):
+    s_len = np.array([64], np.int32)
+    r_len = np.array([60], np.int32)
+    lt = [np.ascontiguousarray(x, dtype=np.int32) for x in lm.interp2(4, 6)]
+    fake = C.c_void_p(0x1000)
+
+    def call(sd=None, rd=None, B=1, sl=s_len, rl=r_len, table=lt, A=fake, rope=None, ws=None, wsb=0,
+             rp=fake):
+        sd = sd or _desc()
+        rd = rd or _desc(L_=6)
+        return L.hf_transfer_kv(B, _p(sl), _p(rl), rp, fake, fake, fake, *[_p(t) for t in table],
+                                C.byref(sd), C.byref(rd), A, None,
+                                C.byref(rope) if rope is not None else None, ws, wsb, None)
+
+    assert call(B=0) == -2
+    assert call(rp=None) == -1
+    assert call(A=None) == -1
+    assert call(sd=_desc(ptr=0)) == -1
+    assert call(sd=_desc(dtype=0)) == -5                       # dtypes differ
+    assert call(sd=_desc(dtype=9)) == -5
+    assert call(sd=_desc(d=64), rd=_desc(L_=6, d=64)) == -8    # bf16 needs d_h = 128
+    assert call(rd=_desc(L_=6, H=3)) == -8                     # receiver heads
+    assert call(sd=_desc(ptr=0x1008)) == -2                    # misaligned
+    assert call(rl=np.array([65], np.int32)) == -2             # longer than T_cap
+    bad = [t.copy() for t in lt]
+    bad[0][2] = 4
+    assert call(table=bad) == -2                               # sender layer out of range
+    bad = [t.copy() for t in lt]
+    bad[2][1] = bad[3][1]
+    assert call(table=bad) == -2                               # rem >= den
+    r, keep = hf.make_rope(5e5, 1e9)
+    assert call(rope=r) == -1                                  # RoPE needs a workspace
+    r2, keep2 = hf.make_rope(-1.0, 1e9)
+    assert call(rope=r2, ws=fake, wsb=1 << 30) == -2
+    # cos/sin tables: 64 sender + 60 receiver positions x 64 pairs x 8 bytes
+    assert L.hf_transfer_workspace_bytes(1, _p(s_len), _p(r_len), C.byref(_desc()),
+                                         C.byref(_desc(L_=6)), C.byref(r)) == 64 * 512 + 60 * 512
+
+
+def test_pack_host_validation(L):
+    fake = C.c_void_p(0x1000)
+    assert L.hf_pack_maps(2, 100, 1024, 1, fake, C.c_void_p(0x100000), None) == -2   # d_r % 32
+    assert L.hf_pack_maps(2, 128, 1024, 3, fake, C.c_void_p(0x100000), None) == -5
+    assert L.hf_pack_maps(2, 128, 1024, 1, None, C.c_void_p(0x100000), None) == -1
+    assert L.hf_pack_maps(2, 128, 128, 1, fake, C.c_void_p(0x1000 + 64), None) == -2  # overlap
+    assert hf.hf_packed_maps_bytes(40, 1024, 1024, 1) == 40 * 2 * 1024 * 1024 * 2
+
+
+def test_profiler_host_calls(L):
+    hf.hf_profiler_enable(False)
+    hf.hf_profiler_reset()
+    assert hf.hf_profiler_query(hf.HF_KERNEL_TRANSFER) == (0.0, 0)
+    with pytest.raises(hf.HeteroFoldError):
+        hf.hf_profiler_query(99)

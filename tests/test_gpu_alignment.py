@@ -1,0 +1,109 @@
+"""GPU alignment parity: the HIP kernels must reproduce the oracle's CSR
+table bit for bit, in both modes, on clean, messy and batched spans."""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import alignment as al
+from paper_2609_32259_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def hf():
+    import torch
+    assert torch.cuda.is_available(), "GPU test needs a GPU"
+    from paper_2609_32259_amd import heterofold
+    heterofold.lib()
+    return heterofold
+
+
+def _run(hf, seg, mode):
+    import torch
+    dev = "cuda"
+    t = lambda a: torch.as_tensor(np.ascontiguousarray(a, np.int32), device=dev)  # noqa: E731
+    out = hf.hf_build_alignment(seg.s_cu, seg.r_cu, t(seg.s_beg), t(seg.s_end), t(seg.r_beg),
+                                t(seg.r_end), mode)
+    torch.cuda.synchronize()
+    rp = out.row_ptr.cpu().numpy()
+    nnz = int(rp[-1])
+    return (rp, out.col[:nnz].cpu().numpy(), out.num[:nnz].cpu().numpy(),
+            out.den[:int(seg.r_cu[-1])].cpu().numpy())
+
+
+def _compare(hf, seg, mode, where):
+    print(f"[gpu-align] {where} mode={mode} B={seg.batch} T_s={seg.s_cu[-1]} T_r={seg.r_cu[-1]}",
+          flush=True)
+    got = _run(hf, seg, mode)
+    exp = al.build_alignment_batched(seg.s_cu, seg.r_cu, seg.s_beg, seg.s_end, seg.r_beg,
+                                     seg.r_end, mode)
+    for name, g, e in zip(("row_ptr", "col", "num", "den"), got, exp):
+        assert g.shape == e.shape, f"{where} {mode} {name}: shape {g.shape} vs {e.shape}"
+        assert np.array_equal(g, e), f"{where} {mode} {name}: first diff at {np.nonzero(g != e)[0][:5]}"
+
+
+@pytest.mark.parametrize("mode", ["overlap", "ta"])
+def test_worked_example(hf, golden_dir, mode):
+    ex = json.load(open(os.path.join(golden_dir, "ta_worked_example.json")))
+    ends = {k: np.asarray(ex[k]["end"], np.int32) for k in ("qwen3", "ministral3")}
+    spans = {k: (np.concatenate([[0], v[:-1]]).astype(np.int32), v) for k, v in ends.items()}
+    for src, dst, key in (("qwen3", "ministral3", "qwen3_to_ministral3"),
+                          ("ministral3", "qwen3", "ministral3_to_qwen3")):
+        seg = synth.concat_segmentations([spans[src] + spans[dst]])
+        rp, col, num, den = _run(hf, seg, mode)
+        if mode == "ta":
+            assert col.tolist() == ex["expected_ta"][key]
+        else:
+            e = ex["expected_overlap"][key]
+            assert rp.tolist() == e["row_ptr"] and col.tolist() == e["col"]
+            assert num.tolist() == e["num"] and den.tolist() == e["den"]
+
+
+@pytest.mark.parametrize("name", list(synth.CONFIGS))
+@pytest.mark.parametrize("mode", ["overlap", "ta"])
+def test_config_segmentations(hf, name, mode):
+    cfg = synth.CONFIGS[name]
+    seg = synth.make_segmentation(cfg, seed=0)
+    _compare(hf, seg, mode, name)
+
+
+@pytest.mark.parametrize("seed", range(3))
+@pytest.mark.parametrize("mode", ["overlap", "ta"])
+def test_messy_batched(hf, seed, mode):
+    rng = np.random.default_rng(1000 + seed)
+    parts = []
+    for n_s, n_r in ((700, 650), (1, 1), (3000, 3100), (50, 0), (257, 513), (5000, 4990)):
+        sb, se = synth.segment_messy(rng, n_s, 1, 6, p_empty=0.1, p_gap=0.1, p_dup_end=0.1)
+        if n_r:
+            rb, re_ = synth.segment_messy(rng, n_r, 1, 9, p_empty=0.1, p_gap=0.1, p_dup_end=0.1)
+        else:
+            rb = re_ = np.zeros(0, np.int32)
+        parts.append((sb, se, rb, re_))
+    seg = synth.concat_segmentations(parts)
+    _compare(hf, seg, mode, f"messy seed={seed}")
+
+
+@pytest.mark.parametrize("mode", ["overlap", "ta"])
+def test_long_rows_and_block_edges(hf, mode):
+    # Receiver tokens spanning many sender tokens, rows straddling workgroup
+    # edges, a receiver sequence longer than the sender's text, all-empty
+    # sender prefix.
+    sb = np.array([0, 0, 0] + list(range(0, 600)), np.int32)
+    se = np.array([0, 0, 0] + list(range(1, 601)), np.int32)
+    rl = np.r_[np.full(255, 1), [200], np.full(300, 1), [50, 30]]
+    re_ = np.cumsum(rl).astype(np.int32)
+    rb = (re_ - rl).astype(np.int32)
+    seg = synth.concat_segmentations([(sb, se, rb, re_)])
+    _compare(hf, seg, mode, "long rows")
+
+
+def test_determinism(hf):
+    seg = synth.make_segmentation(synth.CONFIGS["reverse-b4"], seed=3)
+    a = _run(hf, seg, "overlap")
+    b = _run(hf, seg, "overlap")
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)

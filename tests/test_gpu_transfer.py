@@ -1,0 +1,242 @@
+"""GPU transfer parity: hf_transfer_kv against the fp64 oracle.
+
+Small cases are compared element by element over every layer, role and row
+(several row tiles with a ragged tail); full-size workloads are compared on
+sampled rows, in the launch configuration the benchmark times.  Inputs are
+seeded and synthetic (``paper_2609_32259_amd.synth``)."""
+
+import numpy as np
+import pytest
+
+from oracle import alignment as al
+from oracle import layer_map as lm
+from oracle import transfer as tr
+from paper_2609_32259_amd import synth
+
+from _parity import check_layer
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    assert torch.cuda.is_available(), "GPU test needs a GPU"
+    from paper_2609_32259_amd import heterofold
+    heterofold.lib()
+    return torch
+
+
+def _path(cfg, wl, mode="overlap", rope=None, R=None):
+    from paper_2609_32259_amd.path import TransferPath
+    return TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope if rope is None else rope,
+                        cfg.L_r, cfg.H_r, mode=mode, R=R)
+
+
+def _np64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _oracle_seq(wl, b, mode, rope):
+    cfg = wl.cfg
+    sb, se, rb, re_ = wl.seg.seq(b)
+    csr = al.build_alignment(sb, se, rb, re_, mode)
+    T_s = int(wl.seg.s_len[b])
+    S = _np64(wl.S[b, :, :, :, :T_s, :])
+    rp = None
+    if rope is not None:
+        rp = dict(rope)
+        for k in ("pos0_s", "pos0_r"):
+            rp[k] = 0 if rope.get(k) is None else int(np.asarray(rope[k])[b])
+    return tr.transfer(S, lm.interp2(cfg.L_s, cfg.L_r), csr, _np64(wl.A), _np64(wl.bias), rp,
+                       H_r=cfg.H_r)
+
+
+def _compare_full(torch, cfg, wl, mode="overlap", rope="cfg", qlimited_k=False):
+    rope = wl.rope if rope == "cfg" else rope
+    print(f"[gpu-transfer] {cfg.name} mode={mode} B={wl.seg.batch} T_s={list(wl.seg.s_len)} "
+          f"T_r={list(wl.seg.r_len)} rope={rope is not None}", flush=True)
+    path = _path(cfg, wl, mode, rope)
+    R = path.step()
+    torch.cuda.synchronize()
+    worst = (0.0, 0.0)
+    for b in range(wl.seg.batch):
+        T_r = int(wl.seg.r_len[b])
+        if T_r == 0:
+            continue
+        ref = _oracle_seq(wl, b, mode, rope)
+        got = _np64(R[b, :, :, :, :T_r, :])
+        for l in range(cfg.L_r):
+            for c in range(2):
+                rel, mx = check_layer(got[l, c], ref[l, c], f"{cfg.name} b={b} l={l} c={c}",
+                                      dtype=cfg.dtype, quantization_limited=(qlimited_k and c == 0))
+                worst = (max(worst[0], rel), max(worst[1], mx))
+    print(f"[gpu-transfer]   worst rel-Fro {worst[0]:.3e}, max|err| {worst[1]:.3e}", flush=True)
+    return path
+
+
+# --- fp32 -------------------------------------------------------------------
+
+@pytest.mark.parametrize("mode", ["overlap", "ta"])
+def test_tiny_fp32(torch, mode):
+    cfg = synth.TINY_F32
+    wl = synth.make_workload(cfg, seed=0, device="cuda")
+    _compare_full(torch, cfg, wl, mode)
+
+
+def test_fp32_rope_batched_offsets(torch):
+    cfg = synth.TINY_F32.with_(name="fp32 rope", L_s=3, L_r=5, H_s=2, H_r=3, d_h=64,
+                               n_chars=900, rope=(1.0e4, 5.0e5), batch=3)
+    wl = synth.make_workload(cfg, seed=1, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=np.array([0, 7, 1000], np.int32),
+                             pos0_r=np.array([5, 0, 333], np.int32))
+    _compare_full(torch, cfg, wl, "overlap", rope=rope)
+
+
+# --- bf16, small sizes, every element ----------------------------------------
+
+@pytest.mark.parametrize("mode", ["overlap", "ta"])
+def test_bf16_14b_shape_small(torch, mode):
+    cfg = synth.LLAMA8B_14B_8K.with_(T_s=300)          # 5 row tiles of 64, ragged tail
+    wl = synth.make_workload(cfg, seed=2, device="cuda")
+    _compare_full(torch, cfg, wl, mode)
+
+
+def test_bf16_qwen7b_shape_small(torch):
+    cfg = synth.LLAMA8B_QWEN7B_4K.with_(T_s=500)        # 4 receiver heads: 128-row tiles
+    wl = synth.make_workload(cfg, seed=3, device="cuda")
+    _compare_full(torch, cfg, wl, "overlap", qlimited_k=True)
+
+
+def test_bf16_reverse_batched_ragged(torch):
+    cfg = synth.QWEN7B_LLAMA8B_B4
+    parts = []
+    rng = np.random.default_rng(4)
+    for T in (1, 100, 333, 65):
+        sb, se = synth.segment_tokens(rng, T, *cfg.s_len)
+        rb, re_ = synth.segment_chars(rng, int(se[-1]), *cfg.r_len)
+        parts.append((sb, se, rb, re_))
+    seg = synth.concat_segmentations(parts)
+    S = synth.make_cache(cfg, seg, seed=4, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=4, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=np.array([0, 3, 50, 9], np.int32),
+                             pos0_r=np.array([2, 0, 11, 70], np.int32))
+    wl = synth.Workload(cfg, seg, S, A, bias, rope)
+    _compare_full(torch, cfg, wl, "overlap")
+
+
+def test_bf16_two_receiver_heads(torch):
+    cfg = synth.LLAMA8B_14B_8K.with_(name="8->2 heads", H_r=2, L_r=3, T_s=700)   # 256-row tiles
+    wl = synth.make_workload(cfg, seed=5, device="cuda")
+    _compare_full(torch, cfg, wl, "overlap")
+
+
+def test_bf16_identity_is_bit_exact(torch):
+    cfg = synth.LLAMA8B_14B_8K.with_(name="identity", L_s=3, L_r=3, T_s=200, rope=None)
+    wl = synth.make_workload(cfg, seed=6, device="cuda")
+    seg = synth.concat_segmentations([(wl.seg.s_beg, wl.seg.s_end, wl.seg.s_beg, wl.seg.s_end)])
+    eye = torch.eye(cfg.d_r, dtype=torch.bfloat16, device="cuda")
+    A = eye.expand(cfg.L_r, 2, cfg.d_r, cfg.d_in).contiguous()
+    wl = synth.Workload(cfg, seg, wl.S, A, None, None)
+    for mode in ("overlap", "ta"):
+        path = _path(cfg, wl, mode)
+        R = path.step()
+        torch.cuda.synchronize()
+        assert torch.equal(R[:, :, :, :, :200, :].view(torch.int16),
+                           wl.S[:, :, :, :, :200, :].view(torch.int16))
+
+
+def test_bf16_equal_rope_round_trip(torch):
+    # Same theta and positions on both sides with identity maps: un-rotation
+    # then rotation returns the keys to within one bf16 rounding.
+    cfg = synth.LLAMA8B_14B_8K.with_(name="rope round trip", L_s=2, L_r=2, T_s=150,
+                                     rope=(5.0e5, 5.0e5))
+    wl = synth.make_workload(cfg, seed=7, device="cuda")
+    seg = synth.concat_segmentations([(wl.seg.s_beg, wl.seg.s_end, wl.seg.s_beg, wl.seg.s_end)])
+    A = torch.eye(cfg.d_r, dtype=torch.bfloat16, device="cuda").expand(2, 2, cfg.d_r, cfg.d_in).contiguous()
+    wl = synth.Workload(cfg, seg, wl.S, A, None, synth.rope_params(cfg))
+    R = _path(cfg, wl).step()
+    torch.cuda.synchronize()
+    got, ref = _np64(R[0, :, 0, :, :150, :]), _np64(wl.S[0, :, 0, :, :150, :])
+    # each rounding (of the un-rotated key, then of the output) is at most a
+    # half-ulp of the rotated pair's magnitude
+    pair = np.sqrt(ref[..., :64] ** 2 + ref[..., 64:] ** 2)
+    pair = np.concatenate([pair, pair], axis=-1)
+    assert np.all(np.abs(got - ref) <= 2.0 ** -7 * pair)
+    assert torch.equal(R[0, :, 1, :, :150, :].view(torch.int16), wl.S[0, :, 1, :, :150, :].view(torch.int16))
+
+
+def test_bf16_rows_past_length_untouched_and_deterministic(torch):
+    cfg = synth.LLAMA8B_14B_8K.with_(T_s=260, L_r=4)
+    wl = synth.make_workload(cfg, seed=8, device="cuda")
+    T_r = int(wl.seg.r_len[0])
+    R = torch.full((1, cfg.L_r, 2, cfg.H_r, T_r + 37, cfg.d_h), 7.0, dtype=torch.bfloat16,
+                   device="cuda")
+    path = _path(cfg, wl, R=R)
+    out1 = path.step().clone()
+    out2 = path.step().clone()
+    torch.cuda.synchronize()
+    assert torch.equal(out1.view(torch.int16), out2.view(torch.int16))
+    assert bool((out1[:, :, :, :, T_r:, :] == 7.0).all())
+
+
+# --- bf16, full sizes, sampled rows ------------------------------------------
+
+def _sample_rows(T_r, tile, rng, n=24):
+    rows = {0, 1, T_r - 1, T_r - 2}
+    for t in range(tile, T_r, tile * max(1, (T_r // tile) // 8)):
+        rows.update({t - 1, t})
+    rows.update(rng.integers(0, T_r, n).tolist())
+    return sorted(r for r in rows if 0 <= r < T_r)
+
+
+def _compare_sampled(torch, cfg, wl, layers, mode="overlap", qlimited_k=False, tile=64):
+    print(f"[gpu-transfer] full-size {cfg.name} B={wl.seg.batch} T_s={list(wl.seg.s_len)} "
+          f"T_r={list(wl.seg.r_len)}", flush=True)
+    path = _path(cfg, wl, mode)
+    R = path.step()
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(99)
+    lt = lm.interp2(cfg.L_s, cfg.L_r)
+    A64 = None
+    for b in range(wl.seg.batch):
+        T_r = int(wl.seg.r_len[b])
+        rows = _sample_rows(T_r, tile, rng)
+        csr = al.build_alignment(*wl.seg.seq(b), mode)
+        rp = None
+        if wl.rope is not None:
+            rp = dict(wl.rope, pos0_s=0, pos0_r=0)
+        get = lambda l, c, idx: _np64(wl.S[b, l, c][:, torch.as_tensor(idx, device="cuda"), :])  # noqa: E731
+        for l in layers:
+            for c in (0, 1):
+                A64 = _np64(wl.A[l, c])
+                ref = tr.transfer_rows(get, lt, csr, A64, _np64(wl.bias[l, c]), rp, cfg.d_h, l, c, rows)
+                got = _np64(R[b, l, c][:, torch.as_tensor(rows, device="cuda"), :])
+                check_layer(got, ref, f"{cfg.name} b={b} l={l} c={c} rows={len(rows)}",
+                            quantization_limited=(qlimited_k and c == 0))
+    return path
+
+
+def test_full_qwen7b_shape_4k(torch):
+    cfg = synth.LLAMA8B_QWEN7B_4K
+    wl = synth.make_workload(cfg, seed=0, device="cuda")
+    _compare_sampled(torch, cfg, wl, layers=(0, 1, 13, 27), qlimited_k=True, tile=128)
+
+
+def test_full_14b_shape_8k(torch):
+    cfg = synth.LLAMA8B_14B_8K
+    wl = synth.make_workload(cfg, seed=0, device="cuda")
+    _compare_sampled(torch, cfg, wl, layers=(0, 1, 20, 39))
+
+
+def test_full_14b_shape_32k(torch):
+    cfg = synth.LLAMA8B_14B_32K
+    wl = synth.make_workload(cfg, seed=0, device="cuda")
+    _compare_sampled(torch, cfg, wl, layers=(0, 2, 31, 39))
+
+
+@pytest.mark.parametrize("T", [1024, 16384])
+def test_full_reverse_batch4(torch, T):
+    cfg = synth.QWEN7B_LLAMA8B_B4.with_(T_s=T)
+    wl = synth.make_workload(cfg, seed=0, device="cuda")
+    _compare_sampled(torch, cfg, wl, layers=(0, 5, 31))
