@@ -41,6 +41,28 @@ def _mix(S_lo, S_hi, a_lo, a_hi, rem):
     return m
 
 
+def _weights_matrix(csr, T_s):
+    row_ptr, col, num, den = (np.asarray(t, dtype=np.int64) for t in csr)
+    T_r = row_ptr.size - 1
+    rows = np.repeat(np.arange(T_r), np.diff(row_ptr))
+    w = num.astype(np.float64) / den[rows].astype(np.float64)
+    return sp.csr_matrix((w, col, row_ptr), shape=(T_r, T_s))
+
+
+def features(S, layer_table, csr, rope, layer, role):
+    """Steps 1-3 for one receiver layer and role: the aligned, interpolated,
+    un-rotated flattened sender features x_j, fp64 [T_R, H_S * d_h]."""
+    S = np.asarray(S, dtype=np.float64)
+    _, _, H_s, T_s, d_h = S.shape
+    lo, hi, rem, den_l = (np.asarray(t) for t in layer_table)
+    a_lo, a_hi = interp2_weights(lo, hi, rem, den_l)
+    m = _mix(S[lo[layer], role], S[hi[layer], role], a_lo[layer], a_hi[layer], rem[layer])
+    if role == K and rope is not None and rope.get("unrotate_sender_k", False):
+        m = _rope.unrotate(m, rope.get("pos0_s", 0) + np.arange(T_s), rope["theta_s"])
+    u = m.transpose(1, 0, 2).reshape(T_s, H_s * d_h)                    # head-major
+    return _weights_matrix(csr, T_s) @ u
+
+
 def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None):
     """Whole receiver cache of one sequence.
 
@@ -59,43 +81,30 @@ def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None):
     if d_in != H_s * d_h:
         raise ValueError("A's input size must be H_S * d_h")
     H_r = d_r // d_h if H_r is None else H_r
-    lo, hi, rem, den_l = (np.asarray(t) for t in layer_table)
-    a_lo, a_hi = interp2_weights(lo, hi, rem, den_l)
-    row_ptr, col, num, den = (np.asarray(t, dtype=np.int64) for t in csr)
-    T_r = row_ptr.size - 1
-    rows = np.repeat(np.arange(T_r), np.diff(row_ptr))
-    w = num.astype(np.float64) / den[rows].astype(np.float64)
-    W = sp.csr_matrix((w, col, row_ptr), shape=(T_r, T_s))
-    s_pos = r_pos = None
-    if rope is not None:
-        s_pos = rope.get("pos0_s", 0) + np.arange(T_s)
-        r_pos = rope.get("pos0_r", 0) + np.arange(T_r)
+    T_r = np.asarray(csr[0]).size - 1
     out = np.empty((L_r, 2, H_r, T_r, d_h), dtype=np.float64)
     for l in range(L_r):
         for c in (K, V):
-            m = _mix(S[lo[l], c], S[hi[l], c], a_lo[l], a_hi[l], rem[l])  # [H_s,T_s,d_h]
-            if c == K and rope is not None and rope.get("unrotate_sender_k", False):
-                m = _rope.unrotate(m, s_pos, rope["theta_s"])
-            u = m.transpose(1, 0, 2).reshape(T_s, H_s * d_h)               # head-major
-            x = W @ u                                                       # [T_r, d_S]
+            x = features(S, layer_table, csr, rope, l, c)                  # [T_r, d_S]
             y = x @ A[l, c].T
             if b is not None:
                 y = y + np.asarray(b, dtype=np.float64)[l, c][None, :]
             y = y.reshape(T_r, H_r, d_h).transpose(1, 0, 2)                 # [H_r,T_r,d_h]
             if c == K and rope is not None and rope.get("rotate_receiver_k", False):
-                y = _rope.rotate(y, r_pos, rope["theta_r"])
+                y = _rope.rotate(y, rope.get("pos0_r", 0) + np.arange(T_r), rope["theta_r"])
             out[l, c] = y
     return out
 
 
 def transfer_rows(get_sender, layer_table, csr, A_lc, b_lc, rope, d_h,
-                  layer, role, rows):
+                  layer, role, rows, return_features=False):
     """Selected receiver rows of one (layer, role), entry by entry.
 
     get_sender(l, c, idx) -> fp64 [H_S, len(idx), d_h] gives sender rows idx
     of sender layer l, role c (only the rows the CSR entries name are asked
     for).  A_lc is A[layer, role] ([d_R, d_S]); b_lc its bias or None.
-    Returns fp64 [H_R, len(rows), d_h].
+    Returns fp64 [H_R, len(rows), d_h] (and the features x, fp64
+    [len(rows), d_S], when return_features).
     """
     lo, hi, rem, den_l = (np.asarray(t) for t in layer_table)
     a_lo, a_hi = interp2_weights(lo, hi, rem, den_l)
@@ -105,6 +114,7 @@ def transfer_rows(get_sender, layer_table, csr, A_lc, b_lc, rope, d_h,
     H_r = d_r // d_h
     rows = np.asarray(rows, dtype=np.int64)
     out = np.empty((H_r, rows.size, d_h), dtype=np.float64)
+    xs = np.empty((rows.size, d_in), dtype=np.float64)
     unrot = role == K and rope is not None and rope.get("unrotate_sender_k", False)
     rot = role == K and rope is not None and rope.get("rotate_receiver_k", False)
     for n, j in enumerate(rows):
@@ -121,6 +131,7 @@ def transfer_rows(get_sender, layer_table, csr, A_lc, b_lc, rope, d_h,
                 p = rope.get("pos0_s", 0) + int(col[e])
                 m = _rope.unrotate(m[:, None, :], [p], rope["theta_s"])[:, 0, :]
             x += (float(num[e]) / float(den[j])) * m.reshape(-1)
+        xs[n] = x
         y = A_lc @ x
         if b_lc is not None:
             y = y + np.asarray(b_lc, dtype=np.float64)
@@ -129,4 +140,4 @@ def transfer_rows(get_sender, layer_table, csr, A_lc, b_lc, rope, d_h,
             qpos = rope.get("pos0_r", 0) + int(j)
             y = _rope.rotate(y[:, None, :], [qpos], rope["theta_r"])[:, 0, :]
         out[:, n, :] = y
-    return out
+    return (out, xs) if return_features else out

@@ -1,11 +1,17 @@
 """Tolerance checks shared by the GPU parity tests.
 
 bf16 outputs: per (layer, role), relative Frobenius error <= 5e-3 and max
-elementwise |error| <= 2e-2 against the fp64 oracle.  Where the receiver
-values are large enough that bf16 cannot represent them to 2e-2 at all
-(|y| >= 8 gives a half-ulp of 1/32), the max-abs gate is taken on the error
-beyond the output's own half-ulp ("quantization-limited"); that relaxation is
-only used for the configuration with log-normal outlier key channels.
+elementwise |error| <= 2e-2 against the fp64 oracle.
+
+One workload draws log-normal(0, 1) per-channel key scales, so a few feature
+channels reach |x| ~ 1e2.  There the bf16 representation itself forbids the
+literal max-abs gate: the mapped features are bf16 (half-ulp 0.5 at
+|x| in [128, 256)) and so are the outputs (half-ulp 1/32 at |y| in [8, 16)).
+For that case ("quantization-limited") every element must satisfy
+|error| <= 2e-2, or else lie within the worst-case first-order error of the
+two roundings the arithmetic performs,
+    half_ulp(y) + sum_k |A_nk| half_ulp(x_k)   (+ an fp32 accumulation term),
+which a wrong index, sign or dropped term would exceed.
 fp32 outputs: the same gates, plus relative Frobenius error <= 1e-5.
 """
 
@@ -30,16 +36,29 @@ def err_stats(got, ref):
     return rel, (float(np.max(np.abs(d))) if d.size else 0.0), d
 
 
-def check_layer(got, ref, where, dtype="bf16", quantization_limited=False):
+def rounding_bound(ref, x, A):
+    """Per-element first-order bound of bf16-rounding x and y.
+    ref [H_r, T, d_h] oracle outputs; x [T, d_S] oracle features; A [d_R, d_S]."""
+    H_r, T, d_h = ref.shape
+    Aa = np.abs(np.asarray(A, dtype=np.float64))
+    bx = bf16_half_ulp(x) @ Aa.T                         # [T, d_R]
+    acc = 1e-5 * (np.abs(x) @ Aa.T)                      # fp32 accumulation, generous
+    b = (bx + acc).reshape(T, H_r, d_h).transpose(1, 0, 2)
+    return bf16_half_ulp(np.abs(ref) * (1 + 2.0 ** -7) + b) + b
+
+
+def check_layer(got, ref, where, dtype="bf16", quantization_limited=False, x=None, A=None):
     rel, mx, d = err_stats(got, ref)
     assert np.all(np.isfinite(got)), f"{where}: non-finite output"
     assert rel <= REL_FRO, f"{where}: rel Frobenius {rel:.3e} > {REL_FRO}"
     if dtype == "f32":
         assert rel <= 1e-5, f"{where}: fp32 rel Frobenius {rel:.3e} > 1e-5"
     if quantization_limited:
-        excess = np.abs(d) - bf16_half_ulp(ref)
-        assert float(np.max(excess, initial=0.0)) <= MAX_ABS, \
-            f"{where}: max |err| beyond half-ulp {np.max(excess):.3e} > {MAX_ABS}"
+        assert x is not None and A is not None, "quantization-limited gate needs x and A"
+        bound = rounding_bound(ref, x, A)
+        bad = (np.abs(d) > MAX_ABS) & (np.abs(d) > bound)
+        assert not bad.any(), (f"{where}: {int(bad.sum())} elements beyond both 2e-2 and the "
+                               f"rounding bound; worst |err| {mx:.3e}")
     else:
         assert mx <= MAX_ABS, f"{where}: max |err| {mx:.3e} > {MAX_ABS}"
     return rel, mx

@@ -68,8 +68,18 @@ def _compare_full(torch, cfg, wl, mode="overlap", rope="cfg", qlimited_k=False):
         got = _np64(R[b, :, :, :, :T_r, :])
         for l in range(cfg.L_r):
             for c in range(2):
+                x = A = None
+                ql = qlimited_k and c == 0
+                if ql:
+                    assert rope is None, "the rounding bound assumes no receiver rotation"
+                    sb, se, rb, re_ = wl.seg.seq(b)
+                    csr = al.build_alignment(sb, se, rb, re_, mode)
+                    T_s = int(wl.seg.s_len[b])
+                    x = tr.features(_np64(wl.S[b, :, :, :, :T_s, :]), lm.interp2(cfg.L_s, cfg.L_r),
+                                    csr, None, l, c)
+                    A = _np64(wl.A[l, c])
                 rel, mx = check_layer(got[l, c], ref[l, c], f"{cfg.name} b={b} l={l} c={c}",
-                                      dtype=cfg.dtype, quantization_limited=(qlimited_k and c == 0))
+                                      dtype=cfg.dtype, quantization_limited=ql, x=x, A=A)
                 worst = (max(worst[0], rel), max(worst[1], mx))
     print(f"[gpu-transfer]   worst rel-Fro {worst[0]:.3e}, max|err| {worst[1]:.3e}", flush=True)
     return path
@@ -198,7 +208,6 @@ def _compare_sampled(torch, cfg, wl, layers, mode="overlap", qlimited_k=False, t
     torch.cuda.synchronize()
     rng = np.random.default_rng(99)
     lt = lm.interp2(cfg.L_s, cfg.L_r)
-    A64 = None
     for b in range(wl.seg.batch):
         T_r = int(wl.seg.r_len[b])
         rows = _sample_rows(T_r, tile, rng)
@@ -210,10 +219,11 @@ def _compare_sampled(torch, cfg, wl, layers, mode="overlap", qlimited_k=False, t
         for l in layers:
             for c in (0, 1):
                 A64 = _np64(wl.A[l, c])
-                ref = tr.transfer_rows(get, lt, csr, A64, _np64(wl.bias[l, c]), rp, cfg.d_h, l, c, rows)
+                ref, x = tr.transfer_rows(get, lt, csr, A64, _np64(wl.bias[l, c]), rp, cfg.d_h, l,
+                                          c, rows, return_features=True)
                 got = _np64(R[b, l, c][:, torch.as_tensor(rows, device="cuda"), :])
                 check_layer(got, ref, f"{cfg.name} b={b} l={l} c={c} rows={len(rows)}",
-                            quantization_limited=(qlimited_k and c == 0))
+                            quantization_limited=(qlimited_k and c == 0), x=x, A=A64)
     return path
 
 
