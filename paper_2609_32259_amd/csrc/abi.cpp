@@ -326,10 +326,12 @@ int32_t rope_sizes(int32_t B, const int32_t* s_len, const int32_t* r_len, const 
     if (rope->unrotate_sender_k) rs.P_s = std::max(rs.P_s, (int)(ps + s_len[b]));
     if (rope->rotate_receiver_k) rs.P_r = std::max(rs.P_r, (int)(pr + r_len[b]));
   }
+  // The bf16 kernels also read the rotations of the small offsets 0..15.
+  if (rs.P_s > 0) rs.P_s = std::max(rs.P_s, hf::kRopeDeltaRows);
   return HF_OK;
 }
 
-size_t rope_bytes(int P, int d_h) { return align_up((size_t)P * (d_h / 2) * sizeof(float2), 256); }
+size_t rope_bytes(int P, int d_h) { return align_up((size_t)P * d_h * sizeof(float), 256); }
 
 }  // namespace
 
@@ -446,20 +448,20 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* w = static_cast<char*>(workspace);
   if (rope && rope->unrotate_sender_k && rs.P_s > 0) {
-    a.cs_s = reinterpret_cast<const float2*>(w);
+    a.cs_s = reinterpret_cast<const float*>(w);
     a.unrot = 1;
   }
   if (rope && rope->rotate_receiver_k && rs.P_r > 0) {
-    a.cs_r = reinterpret_cast<const float2*>(w + rope_bytes(rs.P_s, d_h));
+    a.cs_r = reinterpret_cast<const float*>(w + rope_bytes(rs.P_s, d_h));
     a.rot = 1;
   }
   if (tiles == 0) return ok();
   hipError_t e = hipSuccess;
   if (a.unrot || a.rot) {
     TimedLaunch t(HF_KERNEL_ROPE_TABLES, s);
-    if (a.unrot) e = hf::launch_rope_table(const_cast<float2*>(a.cs_s), rs.P_s, d_h, rope->theta_s, s);
+    if (a.unrot) e = hf::launch_rope_table(const_cast<float*>(a.cs_s), rs.P_s, d_h, rope->theta_s, s);
     if (e == hipSuccess && a.rot)
-      e = hf::launch_rope_table(const_cast<float2*>(a.cs_r), rs.P_r, d_h, rope->theta_r, s);
+      e = hf::launch_rope_table(const_cast<float*>(a.cs_r), rs.P_r, d_h, rope->theta_r, s);
   }
   if (e != hipSuccess) return hip_fail(e, "RoPE table launch");
   {

@@ -11,6 +11,7 @@
 namespace hf {
 
 constexpr int kAlignBlock = 256;  // receiver rows per alignment workgroup
+constexpr int kRopeDeltaRows = 16;  // sender RoPE table rows the bf16 kernels always read
 
 struct AlignArgs {
   const int32_t* s_beg;
@@ -49,8 +50,8 @@ struct TransferArgs {
   const int32_t* col;
   const int32_t* num;
   const int32_t* den;
-  const float2* cs_s;   // sender cos/sin table [P_s][d_h/2] or nullptr
-  const float2* cs_r;   // receiver cos/sin table [P_r][d_h/2] or nullptr
+  const float* cs_s;    // sender RoPE table [P_s][d_h]: cos of the d_h/2 angles, then sin
+  const float* cs_r;    // receiver RoPE table [P_r][d_h], same layout
   long long s_sb, s_sl, s_sc, s_sh, s_st;
   long long r_sb, r_sl, r_sc, r_sh, r_st;
   int32_t L_r, H_s, H_r, d_h;
@@ -74,7 +75,7 @@ struct TransferArgs {
 int transfer_rows_per_tile(int dtype, int H_r, int d_in);
 
 hipError_t launch_alignment(const AlignArgs& a, hipStream_t s);
-hipError_t launch_rope_table(float2* tab, int P, int d_h, double theta, hipStream_t s);
+hipError_t launch_rope_table(float* tab, int P, int d_h, double theta, hipStream_t s);
 hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* A, void* Wp,
                             hipStream_t s);
 hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s);

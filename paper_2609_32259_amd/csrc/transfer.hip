@@ -3,6 +3,7 @@
 // mean, then the folded affine map of Eq. 9 with bias and receiver RoPE in
 // the epilogue, written straight into the receiver cache layout).
 #include <hip/hip_runtime.h>
+#include <limits.h>
 
 #include "hf_internal.h"
 
@@ -12,6 +13,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void_t;
 
 // ---------------------------------------------------------------------------
 // bf16 helpers.  bf16 -> f32 is exact (the bf16 bits are the top half of the
@@ -36,10 +38,17 @@ __device__ __forceinline__ uint4 pack8(const float* f) {
   return make_uint4(pack2(f[0], f[1]), pack2(f[2], f[3]), pack2(f[4], f[5]), pack2(f[6], f[7]));
 }
 
+// One 16-byte-per-lane global -> LDS copy: lane l writes 16 bytes at
+// lds_wave_base + 16 l (lds_wave_base must be the same for the whole wave).
+__device__ __forceinline__ void copy16_to_lds(const void* gsrc, void* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(gsrc, (lds_void_t*)lds_wave_base, 16, 0, 0);
+}
+
 // ---------------------------------------------------------------------------
-// RoPE tables: tab[pos][k] = (cos, sin)(pos * theta^(-2k/d)), angle in fp64.
+// RoPE tables: row pos holds cos(pos w_k) for k < d/2, then sin(pos w_k), with
+// w_k = theta^(-2k/d); the angle is formed in fp64.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void rope_table_kernel(float2* tab, int P, int half, int d,
+__global__ __launch_bounds__(256) void rope_table_kernel(float* tab, int P, int half, int d,
                                                          double theta) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (long long)P * half) return;
@@ -48,18 +57,19 @@ __global__ __launch_bounds__(256) void rope_table_kernel(float2* tab, int P, int
   const double ang = (double)pos * w;
   double s, c;
   sincos(ang, &s, &c);
-  tab[idx] = make_float2((float)c, (float)s);
+  tab[(long long)pos * d + k] = (float)c;
+  tab[(long long)pos * d + half + k] = (float)s;
 }
 
 // ---------------------------------------------------------------------------
-// Map packing for the bf16 matrix-core kernel.  One 1 KB fragment holds the
+// Map packing for the bf16 matrix-core kernels.  One 1 KB fragment holds the
 // 32 x 16 block (rows n, columns k) one v_mfma_f32_32x32x16_bf16 consumes as
 // its A operand: lane l holds row n = 32 nb + l%32, columns
 // k = 16 ks + 8 (l/32) + 0..7.  Fragments are ordered [lc][ks][nb], so a wave
 // reads one fragment with a single fully coalesced 16-byte-per-lane load.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void pack_bf16_kernel(const uint16_t* A, uint4* Wp, long long n_frag_lanes,
-                                                        int d_r, int d_in) {
+__global__ __launch_bounds__(256) void pack_bf16_kernel(const uint16_t* A, uint4* Wp,
+                                                        long long n_frag_lanes, int d_r, int d_in) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx >= n_frag_lanes) return;
   const int NB = d_r / 32, KS = d_in / 16;
@@ -80,7 +90,7 @@ __global__ __launch_bounds__(256) void copy_f32_kernel(const float4* A, float4* 
 }
 
 // ---------------------------------------------------------------------------
-// Work decoding shared by both transfer kernels.  Work items run role-major,
+// Work decoding shared by the transfer kernels.  Work items run role-major,
 // then layer, then sequence, then row tile, so the workgroups in flight at
 // any time share one map A[l, c] (kept in L2) and the two sender layers it
 // reads, and consecutive receiver layers reuse a sender layer.
@@ -102,60 +112,473 @@ __device__ __forceinline__ Item decode_item(const TransferArgs& p, int item) {
   return it;
 }
 
-// ---------------------------------------------------------------------------
-// bf16 transfer kernel (d_h = 128).
-//
-// One workgroup = 8 waves computes MT = 64*WM receiver rows x all d_r = 128*WN
-// receiver features of one (layer, role).  Wave (wm, wn) owns rows
-// [64 wm, 64 wm + 64) and receiver head wn.  The contraction over the sender
-// features runs one sender head (128 features) at a time:
-//   build:  all 512 threads form the fp32 aligned/interpolated/un-rotated
-//           features X[MT][128] of that head and store them as bf16 in LDS;
-//   mma:    each wave multiplies its 128 x 64 (features x rows) output block
-//           by that X slice on the matrix cores (operands: packed maps from
-//           global memory as the A operand, X from LDS as the B operand).
-// X is built once per row tile and reused for every output feature.  The
-// accumulator of lane l, tile (mt, nt), register i holds receiver row
-// 32 mt + l%32 and feature 32 nt + 8 (i/4) + 4 (l/32) + i%4 of the head, so
-// a RoPE pair (f, f + 64) sits in tiles nt and nt + 2 of the same lane.
-// The epilogue adds the bias, rotates keys, rounds to bf16 and writes through
-// a per-wave LDS staging area so each global store covers whole 256-byte rows.
-// ---------------------------------------------------------------------------
 constexpr int kDH = 128;
-constexpr int kXS = kDH + 8;  // LDS row stride in bf16 elements (16-byte pad)
+constexpr int kXS = kDH + 8;  // LDS row stride of X / staging, bf16 elements (16-byte pad)
 
+// Per-(layer, role, sequence) constants of the bf16 kernels.
+struct Ctx {
+  const uint16_t* S_lo;   // sender cache at (b, lo, c), head 0, token 0
+  const uint16_t* S_hi;
+  const float* cs_s;      // sender RoPE table row of position pos0_s (nullptr: no un-rotation)
+  float wlo, whi;
+  bool two_tap;
+  int Ts;
+};
+
+__device__ __forceinline__ Ctx make_ctx(const TransferArgs& p, const Item& it) {
+  Ctx x;
+  const uint16_t* Sb = static_cast<const uint16_t*>(p.S) + it.b * p.s_sb + it.c * p.s_sc;
+  x.S_lo = Sb + (long long)p.lo[it.l] * p.s_sl;
+  x.S_hi = Sb + (long long)p.hi[it.l] * p.s_sl;
+  x.cs_s = (it.c == 0 && p.unrot) ? p.cs_s + (long long)p.pos0_s[it.b] * kDH : nullptr;
+  x.wlo = p.wlo[it.l];
+  x.whi = p.whi[it.l];
+  x.two_tap = x.whi != 0.0f;
+  x.Ts = p.Ts[it.b];
+  return x;
+}
+
+// Accumulate the aligned features of one receiver row straight from global
+// memory: x[0..7] = features e0..e0+7 and x[8..15] = e0+64..e0+71 of sender
+// head h (a RoPE pair per index).  Used where the staged path does not apply.
+__device__ __forceinline__ void build_row_global(const TransferArgs& p, const Ctx& cx, int g,
+                                                 int h, int e0, float* x) {
+  const int e_beg = p.row_ptr[g], e_end = p.row_ptr[g + 1];
+  const float dinv = (float)p.den[g];
+  for (int e = e_beg; e < e_end; ++e) {
+    const int i = min(max(p.col[e], 0), cx.Ts - 1);
+    const float w = (float)p.num[e] / dinv;
+    const long long off = h * p.s_sh + (long long)i * p.s_st + e0;
+    const uint4 L0 = *reinterpret_cast<const uint4*>(cx.S_lo + off);
+    const uint4 L1 = *reinterpret_cast<const uint4*>(cx.S_lo + off + 64);
+    uint4 H0 = make_uint4(0, 0, 0, 0), H1 = H0;
+    if (cx.two_tap) {
+      H0 = *reinterpret_cast<const uint4*>(cx.S_hi + off);
+      H1 = *reinterpret_cast<const uint4*>(cx.S_hi + off + 64);
+    }
+    const float a = w * cx.wlo, bq = w * cx.whi;
+    const uint32_t l0[4] = {L0.x, L0.y, L0.z, L0.w}, l1[4] = {L1.x, L1.y, L1.z, L1.w};
+    const uint32_t h0[4] = {H0.x, H0.y, H0.z, H0.w}, h1[4] = {H1.x, H1.y, H1.z, H1.w};
+    float cc[8], ss[8];
+    if (cx.cs_s) {
+      const float* row = cx.cs_s + (long long)i * kDH;
+      const float4 c0 = *reinterpret_cast<const float4*>(row + e0);
+      const float4 c1 = *reinterpret_cast<const float4*>(row + e0 + 4);
+      const float4 s0 = *reinterpret_cast<const float4*>(row + 64 + e0);
+      const float4 s1 = *reinterpret_cast<const float4*>(row + 64 + e0 + 4);
+      cc[0] = c0.x; cc[1] = c0.y; cc[2] = c0.z; cc[3] = c0.w;
+      cc[4] = c1.x; cc[5] = c1.y; cc[6] = c1.z; cc[7] = c1.w;
+      ss[0] = s0.x; ss[1] = s0.y; ss[2] = s0.z; ss[3] = s0.w;
+      ss[4] = s1.x; ss[5] = s1.y; ss[6] = s1.z; ss[7] = s1.w;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      float ma = a * ((u & 1) ? bf_hi(l0[u >> 1]) : bf_lo(l0[u >> 1]));
+      float mb = a * ((u & 1) ? bf_hi(l1[u >> 1]) : bf_lo(l1[u >> 1]));
+      if (cx.two_tap) {
+        ma = fmaf(bq, (u & 1) ? bf_hi(h0[u >> 1]) : bf_lo(h0[u >> 1]), ma);
+        mb = fmaf(bq, (u & 1) ? bf_hi(h1[u >> 1]) : bf_lo(h1[u >> 1]), mb);
+      }
+      if (cx.cs_s) {  // U(p) = R(-p) on the pair (e0 + u, e0 + 64 + u)
+        x[u] = fmaf(ma, cc[u], fmaf(mb, ss[u], x[u]));
+        x[u + 8] = fmaf(mb, cc[u], fmaf(-ma, ss[u], x[u + 8]));
+      } else {
+        x[u] += ma;
+        x[u + 8] += mb;
+      }
+    }
+  }
+}
+
+// Epilogue of one 32-row block of a wave: bias, receiver RoPE on keys, bf16
+// rounding, then a write through the wave's LDS staging rows so that global
+// stores cover whole contiguous row segments.
+//   acc[q]  accumulators of the wave's n-tile q (NTW of them) for these rows;
+//   feat[q] first feature (within the receiver head) of n-tile q;
+//   tiles q and q + NTW/2 hold the RoPE pair (f, f + 64).
+template <int NTW>
+__device__ __forceinline__ void epilogue_rows(const TransferArgs& p, f32x16* acc, const int* feat,
+                                              const float* bias_head, const float* cr, bool rot,
+                                              uint16_t* stage, uint16_t* dst_head, int row_base,
+                                              int Tr, int lane) {
+  const int hi4 = 4 * (lane >> 5);
+  const int mcol = lane & 31;
+  const int j = row_base + mcol;
+  float y[NTW][16];
+#pragma unroll
+  for (int q = 0; q < NTW; ++q)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float4 bv = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (bias_head) bv = *reinterpret_cast<const float4*>(bias_head + feat[q] + 8 * g + hi4);
+      y[q][4 * g + 0] = acc[q][4 * g + 0] + bv.x;
+      y[q][4 * g + 1] = acc[q][4 * g + 1] + bv.y;
+      y[q][4 * g + 2] = acc[q][4 * g + 2] + bv.z;
+      y[q][4 * g + 3] = acc[q][4 * g + 3] + bv.w;
+    }
+  if (rot && j < Tr) {
+    const float* crow = cr + (long long)j * kDH;
+#pragma unroll
+    for (int q = 0; q < NTW / 2; ++q)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int f = feat[q] + 8 * g + hi4;  // < 64
+        const float4 cv = *reinterpret_cast<const float4*>(crow + f);
+        const float4 sv = *reinterpret_cast<const float4*>(crow + 64 + f);
+        const float cc[4] = {cv.x, cv.y, cv.z, cv.w};
+        const float ss[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float a = y[q][4 * g + u], b = y[q + NTW / 2][4 * g + u];
+          y[q][4 * g + u] = fmaf(a, cc[u], -b * ss[u]);
+          y[q + NTW / 2][4 * g + u] = fmaf(b, cc[u], a * ss[u]);
+        }
+      }
+  }
+  // stage row mcol: tile q occupies staging columns [32 q, 32 q + 32)
+#pragma unroll
+  for (int q = 0; q < NTW; ++q)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      uint2 v = make_uint2(pack2(y[q][4 * g], y[q][4 * g + 1]), pack2(y[q][4 * g + 2], y[q][4 * g + 3]));
+      *reinterpret_cast<uint2*>(stage + mcol * kXS + 32 * q + 8 * g + hi4) = v;
+    }
+  // write back: NTW*4 lanes per row, each 16 bytes
+  constexpr int LPR = NTW * 4;
+  constexpr int RPP = 64 / LPR;
+#pragma unroll
+  for (int pass = 0; pass < 32 / RPP; ++pass) {
+    const int rr = pass * RPP + lane / LPR;
+    const int ci = lane % LPR;
+    const uint4 v = *reinterpret_cast<const uint4*>(stage + rr * kXS + 8 * ci);
+    const int jj = row_base + rr;
+    if (jj < Tr)
+      *reinterpret_cast<uint4*>(dst_head + (long long)jj * p.r_st + feat[ci / 4] + 8 * (ci % 4)) = v;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 transfer kernel, tiled (d_h = 128, up to 8 sender heads; NTW = 4 for 8
+// receiver heads, NTW = 2 for 4).
+//
+// One workgroup = 8 waves computes 64 receiver rows x all d_r receiver
+// features of one (layer, role), in three phases:
+//   build: all 512 threads form the whole aligned feature block X[64][d_in]
+//          in fp32 -- gather the tile's CSR entries (staged in LDS), mix the
+//          two sender-layer taps, un-rotate keys, weight and sum -- and store
+//          it once as bf16 in LDS.  Sender rows come straight from global
+//          memory; no matrix-core work is in flight, so nothing waits behind
+//          these loads.  Rows are handed to waves sorted by entry count, so the
+//          8 rows of a wave take the same number of loop trips.
+//   mma:   each wave multiplies its output tiles by X over all d_in/16 k-steps
+//          (v_mfma_f32_32x32x16_bf16: packed map fragment from global memory as
+//          A, X from LDS as B) with a four-deep register prefetch of the map
+//          fragments and no barrier inside the loop.
+//   store: bias, receiver RoPE, bf16 rounding, staged writes.
+// Wave w owns NTW 32-feature tiles of one receiver head (NTW = 4: the whole
+// head w; NTW = 2: tiles {w%2, w%2 + 2} of head w/2), so RoPE pairs
+// (f, f + 64) stay inside a lane; the accumulator of lane l, row block mt,
+// tile q, register i holds receiver row 32 mt + l%32 and feature
+// feat[q] + 8 (i/4) + 4 (l/32) + i%4.
+//
+// The un-rotation of sender row i at position p_i is split as
+// U(p_i) = U(q_r) U(p_i - q_r) with q_r the position of the first sender token
+// of receiver row r: the small-offset rotations U(0..15) sit in LDS and the
+// per-row U(q_r) is applied once to each head's sum.  Tiles whose entry count
+// or in-row sender span exceed what is staged build X entry by entry from the
+// CSR and the full RoPE table in global memory (same results).
+// ---------------------------------------------------------------------------
+constexpr int kEMax = 512;             // CSR entries staged per tile
+constexpr int kDMax = kRopeDeltaRows;  // in-row sender offsets handled with the LDS table
+constexpr int kHMax = 8;               // sender heads held in LDS
+constexpr int kXF = kHMax * kDH + 8;   // LDS row stride of X, bf16 elements (16-byte pad)
+constexpr int kXBytes = 64 * kXF * 2;
+constexpr int kDtBytes = kDMax * kDH * 4;            // U(delta) rows: cos | sin, fp32
+constexpr int kStageBytes = 8 * 32 * kXS * 2;        // epilogue staging (aliases X)
+constexpr int kOffDt = kXBytes;
+constexpr int kOffEnt = kOffDt + kDtBytes;
+constexpr int kEntInts = 65 + 64 * 3 + kEMax * 2 + 4;  // estart, rfirst, perm, cnt, ecol, ew, misc
+constexpr int kSmemBytes = kOffEnt + kEntInts * 4;
+static_assert(kStageBytes <= kXBytes, "staging must fit the X region");
+static_assert(kSmemBytes <= 160 * 1024, "LDS budget");
+
+// Accumulate into x (2 heads x 16 features) the staged-entry sum of one row.
+template <bool TWO_TAP, bool UNROT>
+__device__ __forceinline__ void build_row_staged(const Ctx& cx, const TransferArgs& p, int k0,
+                                                 int k1, const int* ecol, const float* ew,
+                                                 int first, const float* dt, int h0, int nh,
+                                                 int e0, float (*x)[16]) {
+  for (int k = k0; k < k1; ++k) {
+    const int i = ecol[k];
+    const float w = ew[k];
+    const float a = w * cx.wlo, bq = w * cx.whi;
+    float cc[8], ss[8];
+    if (UNROT) {  // U(p_i - q_r); row 0 of the table is the identity
+      const int d = i - first;
+      const float4* drow = reinterpret_cast<const float4*>(dt) + d * 32;
+      const int cw = d & 1;
+      const float4 c0 = drow[((e0 >> 2)) ^ cw], c1 = drow[((e0 >> 2) + 1) ^ cw];
+      const float4 s0 = drow[(16 + (e0 >> 2)) ^ cw], s1 = drow[(17 + (e0 >> 2)) ^ cw];
+      cc[0] = c0.x; cc[1] = c0.y; cc[2] = c0.z; cc[3] = c0.w;
+      cc[4] = c1.x; cc[5] = c1.y; cc[6] = c1.z; cc[7] = c1.w;
+      ss[0] = s0.x; ss[1] = s0.y; ss[2] = s0.z; ss[3] = s0.w;
+      ss[4] = s1.x; ss[5] = s1.y; ss[6] = s1.z; ss[7] = s1.w;
+    }
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      if (hh >= nh) break;
+      const long long off = (h0 + hh) * p.s_sh + (long long)i * p.s_st + e0;
+      const uint4 L0 = *reinterpret_cast<const uint4*>(cx.S_lo + off);
+      const uint4 L1 = *reinterpret_cast<const uint4*>(cx.S_lo + off + 64);
+      uint4 H0, H1;
+      if (TWO_TAP) {
+        H0 = *reinterpret_cast<const uint4*>(cx.S_hi + off);
+        H1 = *reinterpret_cast<const uint4*>(cx.S_hi + off + 64);
+      }
+      const uint32_t l0[4] = {L0.x, L0.y, L0.z, L0.w}, l1[4] = {L1.x, L1.y, L1.z, L1.w};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        float ma = a * ((u & 1) ? bf_hi(l0[u >> 1]) : bf_lo(l0[u >> 1]));
+        float mb = a * ((u & 1) ? bf_hi(l1[u >> 1]) : bf_lo(l1[u >> 1]));
+        if (TWO_TAP) {
+          const uint32_t h0w[4] = {H0.x, H0.y, H0.z, H0.w}, h1w[4] = {H1.x, H1.y, H1.z, H1.w};
+          ma = fmaf(bq, (u & 1) ? bf_hi(h0w[u >> 1]) : bf_lo(h0w[u >> 1]), ma);
+          mb = fmaf(bq, (u & 1) ? bf_hi(h1w[u >> 1]) : bf_lo(h1w[u >> 1]), mb);
+        }
+        if (UNROT) {
+          x[hh][u] = fmaf(ma, cc[u], fmaf(mb, ss[u], x[hh][u]));
+          x[hh][u + 8] = fmaf(mb, cc[u], fmaf(-ma, ss[u], x[hh][u + 8]));
+        } else {
+          x[hh][u] += ma;
+          x[hh][u + 8] += mb;
+        }
+      }
+    }
+  }
+}
+
+template <int NTW>
+__global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const TransferArgs p) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kSmemBytes];
+  uint16_t* Xs = reinterpret_cast<uint16_t*>(smem);
+  float* dt = reinterpret_cast<float*>(smem + kOffDt);
+  int* estart = reinterpret_cast<int*>(smem + kOffEnt);
+  int* rfirst = estart + 65;
+  int* perm = rfirst + 64;
+  int* cnt = perm + 64;
+  int* ecol = cnt + 64;
+  float* ew = reinterpret_cast<float*>(ecol + kEMax);
+  int* flag = reinterpret_cast<int*>(ew + kEMax);  // [0]: a row's sender span is too wide
+
+  const Item it = decode_item(p, blockIdx.x);
+  const Ctx cx = make_ctx(p, it);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Tr = p.Tr[it.b];
+  const int j0 = it.tile * 64;
+  const int nrows = min(64, Tr - j0);
+  const int g0 = p.row0[it.b] + j0;
+  const bool unrot = cx.cs_s != nullptr;
+  const int H = p.H_s;
+
+  // ---- stage the tile's alignment entries ----
+  if (tid <= 64) estart[tid] = p.row_ptr[g0 + min(tid, nrows)];
+  if (tid == 0) flag[0] = 0;
+  if (unrot) {  // U(0..15): rows 0..15 of the sender table, 2 per wave; slot c holds chunk c ^ (r & 1)
+    const int ri = wave * 2 + (lane >> 5);
+    const int c = (lane & 31) ^ (ri & 1);
+    copy16_to_lds(p.cs_s + (long long)ri * kDH + 4 * c, dt + wave * 2 * kDH);
+  }
+  __syncthreads();
+  const int e_base = estart[0];
+  const int nnz = estart[nrows] - e_base;
+  bool staged = nnz <= kEMax;
+  if (staged) {
+    for (int t = tid; t < nnz; t += 512) {
+      int lo = 0, hi = nrows;  // row r with estart[r] <= e_base + t < estart[r + 1]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (estart[mid] <= e_base + t) lo = mid; else hi = mid;
+      }
+      const int e = e_base + t;
+      ecol[t] = min(max(p.col[e], 0), cx.Ts - 1);
+      ew[t] = (float)p.num[e] / (float)p.den[g0 + lo];
+    }
+  }
+  if (tid < 64) cnt[tid] = tid < nrows ? estart[tid + 1] - estart[tid] : 0;
+  __syncthreads();
+  if (tid < 64) {
+    // rank rows by entry count (ties by index): waves then get rows of equal length
+    const int c = cnt[tid];
+    int rank = 0;
+    for (int r = 0; r < 64; ++r) {
+      const int cr = cnt[r];
+      rank += (cr < c) || (cr == c && r < tid);
+    }
+    perm[rank] = tid;
+    if (staged && tid < nrows) {
+      int lmin = INT_MAX, lmax = -1;
+      for (int k = estart[tid] - e_base; k < estart[tid + 1] - e_base; ++k) {
+        lmin = min(lmin, ecol[k]);
+        lmax = max(lmax, ecol[k]);
+      }
+      rfirst[tid] = lmin == INT_MAX ? 0 : lmin;
+      if (lmax - lmin >= kDMax) flag[0] = 1;
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // the U(0..15) table has landed
+  __syncthreads();
+  staged = staged && flag[0] == 0;
+
+  // ---- build X[64][d_in] ----
+  {
+    const int r = perm[tid >> 3];  // 8 threads per row, rows in entry-count order
+    const int e0 = (tid & 7) * 8;   // features e0..e0+7 and e0+64..e0+71 of every head
+    float rc[8], rs[8];             // U(q_r) at the row's base position
+    if (staged && unrot && r < nrows) {
+      const float* row = cx.cs_s + (long long)rfirst[r] * kDH;
+      const float4 c0 = *reinterpret_cast<const float4*>(row + e0);
+      const float4 c1 = *reinterpret_cast<const float4*>(row + e0 + 4);
+      const float4 s0 = *reinterpret_cast<const float4*>(row + 64 + e0);
+      const float4 s1 = *reinterpret_cast<const float4*>(row + 64 + e0 + 4);
+      rc[0] = c0.x; rc[1] = c0.y; rc[2] = c0.z; rc[3] = c0.w;
+      rc[4] = c1.x; rc[5] = c1.y; rc[6] = c1.z; rc[7] = c1.w;
+      rs[0] = s0.x; rs[1] = s0.y; rs[2] = s0.z; rs[3] = s0.w;
+      rs[4] = s1.x; rs[5] = s1.y; rs[6] = s1.z; rs[7] = s1.w;
+    }
+    for (int h0 = 0; h0 < H; h0 += 2) {
+      const int nh = min(2, H - h0);
+      float x[2][16];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int u = 0; u < 16; ++u) x[hh][u] = 0.0f;
+      if (r < nrows) {
+        if (staged) {
+          const int k0 = estart[r] - e_base, k1 = estart[r + 1] - e_base;
+          const int first = rfirst[r];
+          if (cx.two_tap) {
+            if (unrot) build_row_staged<true, true>(cx, p, k0, k1, ecol, ew, first, dt, h0, nh, e0, x);
+            else build_row_staged<true, false>(cx, p, k0, k1, ecol, ew, first, dt, h0, nh, e0, x);
+          } else {
+            if (unrot) build_row_staged<false, true>(cx, p, k0, k1, ecol, ew, first, dt, h0, nh, e0, x);
+            else build_row_staged<false, false>(cx, p, k0, k1, ecol, ew, first, dt, h0, nh, e0, x);
+          }
+          if (unrot) {  // U(q_r) on each head's sum
+#pragma unroll
+            for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                const float a = x[hh][u], b = x[hh][u + 8];
+                x[hh][u] = fmaf(a, rc[u], b * rs[u]);
+                x[hh][u + 8] = fmaf(b, rc[u], -a * rs[u]);
+              }
+          }
+        } else {
+          build_row_global(p, cx, g0 + r, h0, e0, x[0]);
+          if (nh > 1) build_row_global(p, cx, g0 + r, h0 + 1, e0, x[1]);
+        }
+      }
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        if (hh >= nh) break;
+        uint16_t* xr = Xs + r * kXF + (h0 + hh) * kDH;
+        *reinterpret_cast<uint4*>(xr + e0) = pack8(x[hh]);
+        *reinterpret_cast<uint4*>(xr + 64 + e0) = pack8(x[hh] + 8);
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- multiply ----
+  const int head = NTW == 4 ? wave : (wave >> 1);
+  const int nt0 = NTW == 4 ? 0 : (wave & 1);
+  constexpr int NTS = 4 / NTW;  // n-tile stride inside the head
+  int feat[NTW];
+#pragma unroll
+  for (int q = 0; q < NTW; ++q) feat[q] = 32 * (nt0 + q * NTS);
+  const int KS = H * (kDH / 16);
+  const int NB = p.H_r * (kDH / 32);
+  const int lc_store = it.l * 2 + it.c;
+  const bf16x8* W = static_cast<const bf16x8*>(p.Wp) + (long long)lc_store * KS * NB * 64 +
+                    (4 * head + nt0) * 64 + lane;
+
+  f32x16 acc[2][NTW];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int q = 0; q < NTW; ++q)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[mt][q][i] = 0.0f;
+
+  bf16x8 wr[4][NTW];  // map fragments of four consecutive k-steps
+  auto load_w = [&](bf16x8* dst, int ks) {
+    const bf16x8* Wk = W + (long long)ks * NB * 64;
+#pragma unroll
+    for (int q = 0; q < NTW; ++q) dst[q] = Wk[q * NTS * 64];
+  };
+  auto step = [&](bf16x8* wf, int ks) {
+    bf16x8 xa[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+      xa[mt] = *reinterpret_cast<const bf16x8*>(Xs + (32 * mt + (lane & 31)) * kXF + 16 * ks +
+                                                8 * (lane >> 5));
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int q = 0; q < NTW; ++q)
+        acc[mt][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[q], xa[mt], acc[mt][q], 0, 0, 0);
+    if (ks + 4 < KS) load_w(wf, ks + 4);
+  };
+#pragma unroll
+  for (int u = 0; u < 4; ++u) load_w(wr[u], u);  // KS is a multiple of 8
+  for (int ks = 0; ks < KS; ks += 4) {
+    step(wr[0], ks);
+    step(wr[1], ks + 1);
+    step(wr[2], ks + 2);
+    step(wr[3], ks + 3);
+  }
+  __syncthreads();  // every wave is done reading X; LDS becomes staging space
+
+  // ---- store ----
+  uint16_t* stage = Xs + wave * 32 * kXS;
+  uint16_t* dst_head = static_cast<uint16_t*>(p.R) + it.b * p.r_sb + (long long)it.l * p.r_sl +
+                       it.c * p.r_sc + head * p.r_sh;
+  const float* bias_head = p.bias ? p.bias + (long long)lc_store * NB * 32 + head * kDH : nullptr;
+  const bool rot = it.c == 0 && p.rot;
+  const float* cr = rot ? p.cs_r + (long long)p.pos0_r[it.b] * kDH : nullptr;
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+    epilogue_rows<NTW>(p, acc[mt], feat, bias_head, cr, rot, stage, dst_head, j0 + 32 * mt, Tr,
+                       lane);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 transfer kernel, direct (d_h = 128, WN receiver heads): the same
+// computation with X built straight from global memory and one workgroup per
+// 64 (8/WN) rows.  Used for two receiver heads, where a 64-row tile over 8
+// waves would split a RoPE pair across lanes.
+// ---------------------------------------------------------------------------
 template <int WN>
-__global__ __launch_bounds__(512, 1) void transfer_bf16_kernel(const TransferArgs p) {
+__global__ __launch_bounds__(512, 1) void transfer_bf16_direct_kernel(const TransferArgs p) {
   constexpr int WM = 8 / WN;
   constexpr int MT = 64 * WM;
-  constexpr int XBUF = MT * kXS;           // one X buffer, bf16 elements
-  constexpr int STAGE = 32 * kXS;          // one wave's epilogue staging, bf16 elements
+  constexpr int XBUF = MT * kXS;
+  constexpr int STAGE = 32 * kXS;
   constexpr int LDS = (2 * XBUF > 8 * STAGE) ? 2 * XBUF : 8 * STAGE;
   __shared__ __attribute__((aligned(16))) uint16_t lds[LDS];
 
   const Item it = decode_item(p, blockIdx.x);
+  const Ctx cx = make_ctx(p, it);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int j0 = it.tile * MT;
-  const int Tr = p.Tr[it.b], Ts = p.Ts[it.b];
+  const int Tr = p.Tr[it.b];
   const int row0 = p.row0[it.b];
-  const bool keys = it.c == 0;
-  const bool unrot = keys && p.unrot;
-  const bool rot = keys && p.rot;
-  const float wlo = p.wlo[it.l], whi = p.whi[it.l];
-  const bool two_tap = whi != 0.0f;
-  const uint16_t* Sb = static_cast<const uint16_t*>(p.S) + it.b * p.s_sb + it.c * p.s_sc;
-  const uint16_t* S_lo = Sb + (long long)p.lo[it.l] * p.s_sl;
-  const uint16_t* S_hi = Sb + (long long)p.hi[it.l] * p.s_sl;
-  const float2* cs_s = unrot ? p.cs_s + (long long)p.pos0_s[it.b] * (kDH / 2) : nullptr;
-
-  const int KS = p.H_s * (kDH / 16);  // 16-wide k steps over all sender features
-  const int NB = p.H_r * (kDH / 32);  // 32-row fragments over all receiver features
+  const int KS = p.H_s * (kDH / 16);
+  const int NB = p.H_r * (kDH / 32);
   const int lc_store = it.l * 2 + it.c;
-  const bf16x8* W = static_cast<const bf16x8*>(p.Wp) + (long long)lc_store * KS * NB * 64;
-
-  // Build mapping: 8 threads per row, thread owns features e0..e0+7 and
-  // e0+64..e0+71 of the current sender head (a RoPE pair per index).
+  const bf16x8* W = static_cast<const bf16x8*>(p.Wp) + (long long)lc_store * KS * NB * 64 +
+                    (wn * 4) * 64 + lane;
   const int brow = tid >> 3;
   const int e0 = (tid & 7) * 8;
 
@@ -169,57 +592,18 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_kernel(const TransferArg
 
   for (int h = 0; h < p.H_s; ++h) {
     uint16_t* xb = lds + (h & 1) * XBUF;
-    // ---- build X for sender head h ----
 #pragma unroll
     for (int q = 0; q < WM; ++q) {
       const int r = brow + 64 * q;
-      const int j = j0 + r;
       float x[16];
 #pragma unroll
       for (int u = 0; u < 16; ++u) x[u] = 0.0f;
-      if (j < Tr) {
-        const int g = row0 + j;
-        const int e_beg = p.row_ptr[g], e_end = p.row_ptr[g + 1];
-        const float dinv = (float)p.den[g];
-        for (int e = e_beg; e < e_end; ++e) {
-          int i = p.col[e];
-          i = min(max(i, 0), Ts - 1);
-          const float w = (float)p.num[e] / dinv;
-          const long long off = h * p.s_sh + (long long)i * p.s_st + e0;
-          float m[16], t[16];
-          unpack8(*reinterpret_cast<const uint4*>(S_lo + off), m);
-          unpack8(*reinterpret_cast<const uint4*>(S_lo + off + 64), m + 8);
-#pragma unroll
-          for (int u = 0; u < 16; ++u) m[u] *= wlo;
-          if (two_tap) {
-            unpack8(*reinterpret_cast<const uint4*>(S_hi + off), t);
-            unpack8(*reinterpret_cast<const uint4*>(S_hi + off + 64), t + 8);
-#pragma unroll
-            for (int u = 0; u < 16; ++u) m[u] = fmaf(whi, t[u], m[u]);
-          }
-          if (unrot) {
-            const float4* cs = reinterpret_cast<const float4*>(cs_s + (long long)i * (kDH / 2) + e0);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const float4 v = cs[u];  // (cos, sin) of features e0+2u and e0+2u+1
-              const float c0 = v.x, s0 = v.y, c1 = v.z, s1 = v.w;
-              const float a0 = m[2 * u], b0 = m[2 * u + 8], a1 = m[2 * u + 1], b1 = m[2 * u + 9];
-              m[2 * u] = fmaf(a0, c0, b0 * s0);
-              m[2 * u + 8] = fmaf(b0, c0, -a0 * s0);
-              m[2 * u + 1] = fmaf(a1, c1, b1 * s1);
-              m[2 * u + 9] = fmaf(b1, c1, -a1 * s1);
-            }
-          }
-#pragma unroll
-          for (int u = 0; u < 16; ++u) x[u] = fmaf(w, m[u], x[u]);
-        }
-      }
+      if (j0 + r < Tr) build_row_global(p, cx, row0 + j0 + r, h, e0, x);
       *reinterpret_cast<uint4*>(xb + r * kXS + e0) = pack8(x);
       *reinterpret_cast<uint4*>(xb + r * kXS + e0 + 64) = pack8(x + 8);
     }
     __syncthreads();
-    // ---- multiply: 8 k-steps of 16 over this head ----
-    const bf16x8* Wh = W + (long long)h * 8 * NB * 64 + (wn * 4) * 64 + lane;
+    const bf16x8* Wh = W + (long long)h * 8 * NB * 64;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       bf16x8 xa[2], wf[4];
@@ -238,70 +622,17 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_kernel(const TransferArg
   }
   __syncthreads();  // every wave is done reading X; LDS becomes staging space
 
-  // ---- epilogue ----
-  const int hi4 = 4 * (lane >> 5);
-  const int mcol = lane & 31;
-  float bias_v[4][4][4];  // [nt][g][u]: feature 32 nt + 8 g + hi4 + u
-#pragma unroll
-  for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      float4 bv = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (p.bias)
-        bv = *reinterpret_cast<const float4*>(p.bias + (long long)lc_store * NB * 32 + wn * kDH +
-                                              32 * nt + 8 * g + hi4);
-      bias_v[nt][g][0] = bv.x; bias_v[nt][g][1] = bv.y;
-      bias_v[nt][g][2] = bv.z; bias_v[nt][g][3] = bv.w;
-    }
+  const int feat[4] = {0, 32, 64, 96};
   uint16_t* stage = lds + wave * STAGE;
-  uint16_t* Rb = static_cast<uint16_t*>(p.R) + it.b * p.r_sb + (long long)it.l * p.r_sl +
-                 it.c * p.r_sc + wn * p.r_sh;
+  uint16_t* dst_head = static_cast<uint16_t*>(p.R) + it.b * p.r_sb + (long long)it.l * p.r_sl +
+                       it.c * p.r_sc + wn * p.r_sh;
+  const float* bias_head = p.bias ? p.bias + (long long)lc_store * NB * 32 + wn * kDH : nullptr;
+  const bool rot = it.c == 0 && p.rot;
+  const float* cr = rot ? p.cs_r + (long long)p.pos0_r[it.b] * kDH : nullptr;
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt) {
-    const int rloc = 64 * wm + 32 * mt + mcol;  // row within the tile held by this lane
-    const int j = j0 + rloc;
-    float y[4][16];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) y[nt][i] = acc[mt][nt][i] + bias_v[nt][i >> 2][i & 3];
-    if (rot && j < Tr) {
-      const float2* cr = p.cs_r + (long long)(p.pos0_r[it.b] + j) * (kDH / 2);
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const float4* cp = reinterpret_cast<const float4*>(cr + 32 * nt + 8 * g + hi4);
-          const float4 v0 = cp[0], v1 = cp[1];
-          const float cc[4] = {v0.x, v0.z, v1.x, v1.z};
-          const float ss[4] = {v0.y, v0.w, v1.y, v1.w};
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const float a = y[nt][4 * g + u], bq = y[nt + 2][4 * g + u];
-            y[nt][4 * g + u] = fmaf(a, cc[u], -bq * ss[u]);
-            y[nt + 2][4 * g + u] = fmaf(bq, cc[u], a * ss[u]);
-          }
-        }
-    }
-    // stage: row mcol, features 32 nt + 8 g + hi4 .. +3
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        uint2 v = make_uint2(pack2(y[nt][4 * g], y[nt][4 * g + 1]),
-                             pack2(y[nt][4 * g + 2], y[nt][4 * g + 3]));
-        *reinterpret_cast<uint2*>(stage + mcol * kXS + 32 * nt + 8 * g + hi4) = v;
-      }
-    // write back 32 rows x 256 bytes: 16 lanes per row, 4 rows per pass
-#pragma unroll
-    for (int pass = 0; pass < 8; ++pass) {
-      const int rr = pass * 4 + (lane >> 4);
-      const int cc = (lane & 15) * 8;
-      const uint4 v = *reinterpret_cast<const uint4*>(stage + rr * kXS + cc);
-      const int jj = j0 + 64 * wm + 32 * mt + rr;
-      if (jj < Tr) *reinterpret_cast<uint4*>(Rb + (long long)jj * p.r_st + cc) = v;
-    }
-  }
+  for (int mt = 0; mt < 2; ++mt)
+    epilogue_rows<4>(p, acc[mt], feat, bias_head, cr, rot, stage, dst_head,
+                     j0 + 64 * wm + 32 * mt, Tr, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -346,9 +677,10 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
           m2 = fmaf(whi, S_hi[off + half], m2);
         }
         if (unrot) {
-          const float2 cs = p.cs_s[(long long)(p.pos0_s[it.b] + i) * half + f];
-          const float u1 = fmaf(m1, cs.x, m2 * cs.y);
-          const float u2 = fmaf(m2, cs.x, -m1 * cs.y);
+          const float* cs = p.cs_s + (long long)(p.pos0_s[it.b] + i) * d;
+          const float c = cs[f], s = cs[half + f];
+          const float u1 = fmaf(m1, c, m2 * s);
+          const float u2 = fmaf(m2, c, -m1 * s);
           m1 = u1;
           m2 = u2;
         }
@@ -391,9 +723,10 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
       if (r >= RT || j >= Tr) continue;
       float v1 = y1[r] + b1, v2 = y2[r] + b2;
       if (rot) {
-        const float2 cs = p.cs_r[(long long)(p.pos0_r[it.b] + j) * half + f];
-        const float u1 = fmaf(v1, cs.x, -v2 * cs.y);
-        const float u2 = fmaf(v2, cs.x, v1 * cs.y);
+        const float* cs = p.cs_r + (long long)(p.pos0_r[it.b] + j) * d;
+        const float c = cs[f], s = cs[half + f];
+        const float u1 = fmaf(v1, c, -v2 * s);
+        const float u2 = fmaf(v2, c, v1 * s);
         v1 = u1;
         v2 = u2;
       }
@@ -407,12 +740,13 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
 }  // namespace
 
 int transfer_rows_per_tile(int dtype, int H_r, int d_in) {
-  if (dtype == HF_BF16) return 64 * (8 / (H_r > 0 ? H_r : 1));
+  if (dtype == HF_BF16)
+    return ((H_r == 4 || H_r == 8) && d_in <= kHMax * kDH) ? 64 : 64 * (8 / (H_r > 0 ? H_r : 1));
   int rt = 8192 / (d_in > 0 ? d_in : 1);  // fp32 X tile <= 32 KB of LDS
   return rt < 1 ? 1 : (rt > 16 ? 16 : rt);
 }
 
-hipError_t launch_rope_table(float2* tab, int P, int d_h, double theta, hipStream_t s) {
+hipError_t launch_rope_table(float* tab, int P, int d_h, double theta, hipStream_t s) {
   const int half = d_h / 2;
   const long long n = (long long)P * half;
   if (n <= 0) return hipSuccess;
@@ -443,9 +777,15 @@ hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)items);
   if (dtype == HF_BF16) {
     switch (a.H_r) {
-      case 2: hipLaunchKernelGGL(transfer_bf16_kernel<2>, grid, dim3(512), 0, s, a); break;
-      case 4: hipLaunchKernelGGL(transfer_bf16_kernel<4>, grid, dim3(512), 0, s, a); break;
-      case 8: hipLaunchKernelGGL(transfer_bf16_kernel<8>, grid, dim3(512), 0, s, a); break;
+      case 2: hipLaunchKernelGGL(transfer_bf16_direct_kernel<2>, grid, dim3(512), 0, s, a); break;
+      case 4:
+        if (a.H_s <= kHMax) hipLaunchKernelGGL(transfer_bf16_tiled_kernel<2>, grid, dim3(512), 0, s, a);
+        else hipLaunchKernelGGL(transfer_bf16_direct_kernel<4>, grid, dim3(512), 0, s, a);
+        break;
+      case 8:
+        if (a.H_s <= kHMax) hipLaunchKernelGGL(transfer_bf16_tiled_kernel<4>, grid, dim3(512), 0, s, a);
+        else hipLaunchKernelGGL(transfer_bf16_direct_kernel<8>, grid, dim3(512), 0, s, a);
+        break;
       default: return hipErrorInvalidValue;
     }
   } else {

@@ -135,6 +135,30 @@ def test_bf16_reverse_batched_ragged(torch):
     _compare_full(torch, cfg, wl, "overlap")
 
 
+@pytest.mark.parametrize("H_r", [8, 4])
+def test_bf16_tiles_beyond_staging_capacity(torch, H_r):
+    # Long receiver tokens over short sender tokens make some 64-row tiles read
+    # more sender rows than the LDS staging holds; those tiles take the
+    # global-memory build.  Mixed with ordinary tiles in one launch.
+    cfg = synth.LLAMA8B_14B_8K.with_(name=f"unstaged H_r={H_r}", H_r=H_r, L_r=3)
+    rng = np.random.default_rng(11)
+    sb1, se1 = synth.segment_tokens(rng, 200, 1, 7)
+    sb2, se2 = synth.segment_tokens(rng, 900, 1, 2)
+    sb = np.concatenate([sb1, sb2 + se1[-1]]).astype(np.int32)
+    se = np.concatenate([se1, se2 + se1[-1]]).astype(np.int32)
+    rb1, re1 = synth.segment_chars(rng, int(se1[-1]), 1, 8)
+    rl = rng.integers(8, 17, 400)
+    re2 = (np.cumsum(rl) + se1[-1]).astype(np.int32)
+    re2 = re2[re2 <= se[-1]]
+    rb2 = np.concatenate([[se1[-1]], re2[:-1]]).astype(np.int32)
+    seg = synth.concat_segmentations([(sb, se, np.concatenate([rb1, rb2]).astype(np.int32),
+                                       np.concatenate([re1, re2]).astype(np.int32))])
+    S = synth.make_cache(cfg, seg, seed=11, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=11, device="cuda")
+    wl = synth.Workload(cfg, seg, S, A, bias, synth.rope_params(cfg))
+    _compare_full(torch, cfg, wl, "overlap")
+
+
 def test_bf16_two_receiver_heads(torch):
     cfg = synth.LLAMA8B_14B_8K.with_(name="8->2 heads", H_r=2, L_r=3, T_s=700)   # 256-row tiles
     wl = synth.make_workload(cfg, seed=5, device="cuda")
