@@ -437,6 +437,13 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
     a.pos0_r[b] = rope && rope->pos0_r ? rope->pos0_r[b] : 0;
   }
   a.tile_start[B] = tiles;
+  {  // bytes one (sequence, layer, role) slab of the sender cache spans
+    int Tmax = 1;
+    for (int b = 0; b < B; ++b) Tmax = std::max(Tmax, (int)s_len[b]);
+    const int64_t ext = ((int64_t)(sender->H - 1) * sender->stride_h +
+                         (int64_t)(Tmax - 1) * sender->stride_t + d_h) * (dtype == HF_BF16 ? 2 : 4);
+    a.s_extent = ext < ((int64_t)1 << 31) - 4096 ? (int32_t)ext : 0;
+  }
   a.tiles_per_lc = tiles;
   if ((int64_t)tiles * L_r * 2 > INT32_MAX) return fail(HF_ERR_SHAPE, "too many work items");
   for (int j = 0; j < L_r; ++j) {

@@ -56,6 +56,8 @@ struct TransferArgs {
   long long r_sb, r_sl, r_sc, r_sh, r_st;
   int32_t L_r, H_s, H_r, d_h;
   int32_t unrot, rot;       // RoPE on keys: un-rotate sender / rotate receiver
+  int32_t s_extent;         // bytes spanned by one (sequence, layer, role) slab of the
+                            // sender cache; 0 if that is 2^31 or more
   int32_t B;
   int32_t rows_per_tile;
   int32_t tiles_per_lc;     // row tiles of one (layer, role), summed over the batch

@@ -267,14 +267,18 @@ __device__ __forceinline__ void epilogue_rows(const TransferArgs& p, f32x16* acc
 //          in fp32 -- gather the tile's CSR entries (staged in LDS), mix the
 //          two sender-layer taps, un-rotate keys, weight and sum -- and store
 //          it once as bf16 in LDS.  Sender rows come straight from global
-//          memory; no matrix-core work is in flight, so nothing waits behind
-//          these loads.  Rows are handed to waves sorted by entry count, so the
-//          8 rows of a wave take the same number of loop trips.
+//          memory through a two-stage register pipeline; no matrix-core work is
+//          in flight, so nothing waits behind these loads.  Rows are handed to
+//          waves sorted by entry count, so the 8 rows of a wave take the same
+//          number of loop trips.
 //   mma:   each wave multiplies its output tiles by X over all d_in/16 k-steps
 //          (v_mfma_f32_32x32x16_bf16: packed map fragment from global memory as
 //          A, X from LDS as B) with a four-deep register prefetch of the map
-//          fragments and no barrier inside the loop.
-//   store: bias, receiver RoPE, bf16 rounding, staged writes.
+//          fragments and no barrier inside the loop.  Workgroups start the loop
+//          at different sender heads so that concurrent workgroups stream
+//          different parts of the map.
+//   store: the tile's receiver RoPE rows and the bias are copied into LDS
+//          once; bias, rotation and bf16 rounding, then staged row writes.
 // Wave w owns NTW 32-feature tiles of one receiver head (NTW = 4: the whole
 // head w; NTW = 2: tiles {w%2, w%2 + 2} of head w/2), so RoPE pairs
 // (f, f + 64) stay inside a lane; the accumulator of lane l, row block mt,
@@ -294,65 +298,187 @@ constexpr int kHMax = 8;               // sender heads held in LDS
 constexpr int kXF = kHMax * kDH + 8;   // LDS row stride of X, bf16 elements (16-byte pad)
 constexpr int kXBytes = 64 * kXF * 2;
 constexpr int kDtBytes = kDMax * kDH * 4;            // U(delta) rows: cos | sin, fp32
-constexpr int kStageBytes = 8 * 32 * kXS * 2;        // epilogue staging (aliases X)
 constexpr int kOffDt = kXBytes;
 constexpr int kOffEnt = kOffDt + kDtBytes;
-constexpr int kEntInts = 65 + 64 * 3 + kEMax * 2 + 4;  // estart, rfirst, perm, cnt, ecol, ew, misc
+constexpr int kEntInts = 65 + 64 + kEMax * 3 + 4;    // estart, gbase, ecol, ew, einfo, misc
 constexpr int kSmemBytes = kOffEnt + kEntInts * 4;
-static_assert(kStageBytes <= kXBytes, "staging must fit the X region");
+// Store phase, inside the (then free) X region: receiver RoPE rows, bias, staging.
+constexpr int kOffRcs = 0;                           // [64][cos 64 | sin 64] fp32
+constexpr int kOffBias = kOffRcs + 64 * kDH * 4;     // [d_r <= 1024] fp32
+constexpr int kOffStage = kOffBias + 1024 * 4;       // 8 waves x [32][kXS] bf16
+static_assert(kOffStage + 8 * 32 * kXS * 2 <= kXBytes, "store phase must fit the X region");
 static_assert(kSmemBytes <= 160 * 1024, "LDS budget");
 
-// Accumulate into x (2 heads x 16 features) the staged-entry sum of one row.
-template <bool TWO_TAP, bool UNROT>
-__device__ __forceinline__ void build_row_staged(const Ctx& cx, const TransferArgs& p, int k0,
-                                                 int k1, const int* ecol, const float* ew,
-                                                 int first, const float* dt, int h0, int nh,
-                                                 int e0, float (*x)[16]) {
-  for (int k = k0; k < k1; ++k) {
-    const int i = ecol[k];
-    const float w = ew[k];
-    const float a = w * cx.wlo, bq = w * cx.whi;
-    float cc[8], ss[8];
-    if (UNROT) {  // U(p_i - q_r); row 0 of the table is the identity
-      const int d = i - first;
-      const float4* drow = reinterpret_cast<const float4*>(dt) + d * 32;
-      const int cw = d & 1;
-      const float4 c0 = drow[((e0 >> 2)) ^ cw], c1 = drow[((e0 >> 2) + 1) ^ cw];
-      const float4 s0 = drow[(16 + (e0 >> 2)) ^ cw], s1 = drow[(17 + (e0 >> 2)) ^ cw];
-      cc[0] = c0.x; cc[1] = c0.y; cc[2] = c0.z; cc[3] = c0.w;
-      cc[4] = c1.x; cc[5] = c1.y; cc[6] = c1.z; cc[7] = c1.w;
-      ss[0] = s0.x; ss[1] = s0.y; ss[2] = s0.z; ss[3] = s0.w;
-      ss[4] = s1.x; ss[5] = s1.y; ss[6] = s1.z; ss[7] = s1.w;
+// Group-walk build.  Wave w builds sender head w / WPH for 8 RPG consecutive
+// tile rows (WPH = 8 / RPG waves share a head); lane group g (8 lanes, 16
+// features each) walks the CSR entries of RPG consecutive rows in order, one
+// entry per trip.  An entry whose sender token equals the previous entry's
+// (rows that share a boundary token, forward-filled TA rows) reuses the mixed
+// features already in registers; its loads use an out-of-range buffer offset,
+// which returns zeros without touching memory, so every trip issues the same
+// loads and a ring of R trips keeps R - 1 trips of loads in flight.
+constexpr int kOOB = (int)0x80000000;  // buffer offset past any slab extent (extents < 2^31)
+
+struct GroupLds {
+  const int* estart;  // [65] CSR offsets of the tile rows
+  const int* gbase;   // [64] smallest sender index of each row's group
+  const int* ecol;    // staged sender indices
+  const float* ew;    // staged weights num / den
+  const int* einfo;   // staged row | last-entry-of-row << 8
+  const float* dt;    // U(0..15), swizzled
+  int e_base;
+};
+
+template <bool TWO_TAP>
+struct Trip {
+  uint4 a0, a1, b0, b1;  // tap lo / hi: features e0..e0+7 and e0+64..e0+71
+  int code;              // -1: no entry; else row | last << 6 | dup << 7 | (i - base) << 8
+  float w;
+};
+
+// Rotation rows of the swizzled U(0..15) table: row t holds cos chunks 0..15
+// then sin chunks 16..31 (4 floats each), chunk c stored at slot c ^ (t & 1).
+__device__ __forceinline__ void table_row(const float* tab, int t, int e0, float* c, float* s) {
+  const float4* row = reinterpret_cast<const float4*>(tab) + t * 32;
+  const int cw = t & 1;
+  const float4 c0 = row[(e0 >> 2) ^ cw], c1 = row[((e0 >> 2) + 1) ^ cw];
+  const float4 s0 = row[(16 + (e0 >> 2)) ^ cw], s1 = row[(17 + (e0 >> 2)) ^ cw];
+  c[0] = c0.x; c[1] = c0.y; c[2] = c0.z; c[3] = c0.w;
+  c[4] = c1.x; c[5] = c1.y; c[6] = c1.z; c[7] = c1.w;
+  s[0] = s0.x; s[1] = s0.y; s[2] = s0.z; s[3] = s0.w;
+  s[4] = s1.x; s[5] = s1.y; s[6] = s1.z; s[7] = s1.w;
+}
+
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
+template <bool TWO_TAP, bool UNROT, int R>
+__device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& p, const GroupLds& L,
+                                             int head, int r_first, int rpg, int lane,
+                                             uint16_t* Xs) {
+  const int e0 = (lane & 7) * 8;
+  const int kb = L.estart[r_first] - L.e_base;
+  const int E = L.estart[r_first + rpg] - L.e_base - kb;
+  int T = 0;  // trips of the wave: the longest group
+#pragma unroll
+  for (int g = 0; g < 8; ++g) T = max(T, __builtin_amdgcn_readlane(E, 8 * g));
+  const int base = L.gbase[r_first];
+  for (int q = 0; q < rpg; ++q) {  // rows without entries stay zero
+    const int r = r_first + q;
+    if (L.estart[r + 1] == L.estart[r]) {
+      uint16_t* xr = Xs + r * kXF + head * kDH;
+      *reinterpret_cast<uint4*>(xr + e0) = make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(xr + 64 + e0) = make_uint4(0, 0, 0, 0);
+    }
+  }
+  float rc[8], rs[8];  // U(p_base): closes every row of the group
+  if (UNROT) {
+    const float* row = cx.cs_s + (long long)base * kDH;
+    const float4 c0 = *reinterpret_cast<const float4*>(row + e0);
+    const float4 c1 = *reinterpret_cast<const float4*>(row + e0 + 4);
+    const float4 s0 = *reinterpret_cast<const float4*>(row + 64 + e0);
+    const float4 s1 = *reinterpret_cast<const float4*>(row + 64 + e0 + 4);
+    rc[0] = c0.x; rc[1] = c0.y; rc[2] = c0.z; rc[3] = c0.w;
+    rc[4] = c1.x; rc[5] = c1.y; rc[6] = c1.z; rc[7] = c1.w;
+    rs[0] = s0.x; rs[1] = s0.y; rs[2] = s0.z; rs[3] = s0.w;
+    rs[4] = s1.x; rs[5] = s1.y; rs[6] = s1.z; rs[7] = s1.w;
+  }
+  const __amdgpu_buffer_rsrc_t rlo =
+      __builtin_amdgcn_make_buffer_rsrc((void*)cx.S_lo, 0, p.s_extent, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rhi =
+      __builtin_amdgcn_make_buffer_rsrc((void*)cx.S_hi, 0, p.s_extent, 0x00020000);
+  const int hoff = (int)(head * p.s_sh + e0) * 2;  // bytes
+  const int tstride = (int)p.s_st * 2;
+
+  int iprev = -1;
+  Trip<TWO_TAP> ring[R];
+  float x[16], mp[16];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) x[u] = mp[u] = 0.0f;
+
+  auto issue = [&](Trip<TWO_TAP>& t, int k) {
+    const bool valid = k < E;
+    int i = iprev, info = 0;
+    float w = 0.0f;
+    if (valid) {
+      i = L.ecol[kb + k];
+      w = L.ew[kb + k];
+      info = L.einfo[kb + k];
+    }
+    const bool dup = i == iprev;
+    iprev = i;
+    const int off = dup ? kOOB : hoff + i * tstride;
+    t.a0 = buf_load16(rlo, off);
+    t.a1 = buf_load16(rlo, off + 128);
+    if (TWO_TAP) {
+      t.b0 = buf_load16(rhi, off);
+      t.b1 = buf_load16(rhi, off + 128);
+    }
+    t.code = valid ? ((info & 63) | ((info >> 8) << 6) | ((int)dup << 7) | ((UNROT ? i - base : 0) << 8))
+                   : -1;
+    t.w = w;
+  };
+  auto consume = [&](const Trip<TWO_TAP>& t) {
+    if (t.code < 0) return;
+    const bool dup = (t.code >> 7) & 1;
+    const uint32_t l0[4] = {t.a0.x, t.a0.y, t.a0.z, t.a0.w};
+    const uint32_t l1[4] = {t.a1.x, t.a1.y, t.a1.z, t.a1.w};
+    uint32_t h0[4] = {0, 0, 0, 0}, h1[4] = {0, 0, 0, 0};
+    if (TWO_TAP) {
+      h0[0] = t.b0.x; h0[1] = t.b0.y; h0[2] = t.b0.z; h0[3] = t.b0.w;
+      h1[0] = t.b1.x; h1[1] = t.b1.y; h1[2] = t.b1.z; h1[3] = t.b1.w;
     }
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      if (hh >= nh) break;
-      const long long off = (h0 + hh) * p.s_sh + (long long)i * p.s_st + e0;
-      const uint4 L0 = *reinterpret_cast<const uint4*>(cx.S_lo + off);
-      const uint4 L1 = *reinterpret_cast<const uint4*>(cx.S_lo + off + 64);
-      uint4 H0, H1;
+    for (int u = 0; u < 8; ++u) {  // layer mix of this token, or the previous token's
+      float ma = cx.wlo * ((u & 1) ? bf_hi(l0[u >> 1]) : bf_lo(l0[u >> 1]));
+      float mb = cx.wlo * ((u & 1) ? bf_hi(l1[u >> 1]) : bf_lo(l1[u >> 1]));
       if (TWO_TAP) {
-        H0 = *reinterpret_cast<const uint4*>(cx.S_hi + off);
-        H1 = *reinterpret_cast<const uint4*>(cx.S_hi + off + 64);
+        ma = fmaf(cx.whi, (u & 1) ? bf_hi(h0[u >> 1]) : bf_lo(h0[u >> 1]), ma);
+        mb = fmaf(cx.whi, (u & 1) ? bf_hi(h1[u >> 1]) : bf_lo(h1[u >> 1]), mb);
       }
-      const uint32_t l0[4] = {L0.x, L0.y, L0.z, L0.w}, l1[4] = {L1.x, L1.y, L1.z, L1.w};
+      mp[u] = dup ? mp[u] : ma;
+      mp[u + 8] = dup ? mp[u + 8] : mb;
+    }
+    const float w = t.w;
+    if (UNROT) {  // x += w U(p_i - p_base) m
+      float cc[8], ss[8];
+      table_row(L.dt, t.code >> 8, e0, cc, ss);
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        float ma = a * ((u & 1) ? bf_hi(l0[u >> 1]) : bf_lo(l0[u >> 1]));
-        float mb = a * ((u & 1) ? bf_hi(l1[u >> 1]) : bf_lo(l1[u >> 1]));
-        if (TWO_TAP) {
-          const uint32_t h0w[4] = {H0.x, H0.y, H0.z, H0.w}, h1w[4] = {H1.x, H1.y, H1.z, H1.w};
-          ma = fmaf(bq, (u & 1) ? bf_hi(h0w[u >> 1]) : bf_lo(h0w[u >> 1]), ma);
-          mb = fmaf(bq, (u & 1) ? bf_hi(h1w[u >> 1]) : bf_lo(h1w[u >> 1]), mb);
-        }
-        if (UNROT) {
-          x[hh][u] = fmaf(ma, cc[u], fmaf(mb, ss[u], x[hh][u]));
-          x[hh][u + 8] = fmaf(mb, cc[u], fmaf(-ma, ss[u], x[hh][u + 8]));
-        } else {
-          x[hh][u] += ma;
-          x[hh][u + 8] += mb;
+        const float ma = w * mp[u], mb = w * mp[u + 8];
+        x[u] = fmaf(ma, cc[u], fmaf(mb, ss[u], x[u]));
+        x[u + 8] = fmaf(mb, cc[u], fmaf(-ma, ss[u], x[u + 8]));
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = fmaf(w, mp[u], x[u]);
+    }
+    if ((t.code >> 6) & 1) {  // last entry of the row: close the rotation, round, store
+      if (UNROT) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const float a = x[u], b = x[u + 8];
+          x[u] = fmaf(a, rc[u], b * rs[u]);
+          x[u + 8] = fmaf(b, rc[u], -a * rs[u]);
         }
       }
+      uint16_t* xr = Xs + (t.code & 63) * kXF + head * kDH;
+      *reinterpret_cast<uint4*>(xr + e0) = pack8(x);
+      *reinterpret_cast<uint4*>(xr + 64 + e0) = pack8(x + 8);
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = 0.0f;
+    }
+  };
+
+#pragma unroll
+  for (int s = 0; s < R - 1; ++s) issue(ring[s], s);
+  for (int t0 = 0; t0 < T; t0 += R) {
+#pragma unroll
+    for (int s = 0; s < R; ++s) {
+      issue(ring[(s + R - 1) % R], t0 + s + R - 1);
+      if (t0 + s < T) consume(ring[s]);
     }
   }
 }
@@ -363,12 +489,11 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   uint16_t* Xs = reinterpret_cast<uint16_t*>(smem);
   float* dt = reinterpret_cast<float*>(smem + kOffDt);
   int* estart = reinterpret_cast<int*>(smem + kOffEnt);
-  int* rfirst = estart + 65;
-  int* perm = rfirst + 64;
-  int* cnt = perm + 64;
-  int* ecol = cnt + 64;
+  int* gbase = estart + 65;
+  int* ecol = gbase + 64;
   float* ew = reinterpret_cast<float*>(ecol + kEMax);
-  int* flag = reinterpret_cast<int*>(ew + kEMax);  // [0]: a row's sender span is too wide
+  int* einfo = reinterpret_cast<int*>(ew + kEMax);
+  int* flag = einfo + kEMax;  // [0]: the staged build does not apply
 
   const Item it = decode_item(p, blockIdx.x);
   const Ctx cx = make_ctx(p, it);
@@ -379,11 +504,14 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   const int g0 = p.row0[it.b] + j0;
   const bool unrot = cx.cs_s != nullptr;
   const int H = p.H_s;
+  // WPH waves share a sender head; a lane group walks RPG consecutive rows
+  const int WPH = H == 1 ? 8 : H == 2 ? 4 : H <= 4 ? 2 : 1;
+  const int RPG = 8 / WPH;
 
   // ---- stage the tile's alignment entries ----
   if (tid <= 64) estart[tid] = p.row_ptr[g0 + min(tid, nrows)];
-  if (tid == 0) flag[0] = 0;
-  if (unrot) {  // U(0..15): rows 0..15 of the sender table, 2 per wave; slot c holds chunk c ^ (r & 1)
+  if (tid == 0) flag[0] = p.s_extent > 0 ? 0 : 1;
+  if (unrot) {  // U(0..15): rows 0..15 of the sender table, 2 per wave
     const int ri = wave * 2 + (lane >> 5);
     const int c = (lane & 31) ^ (ri & 1);
     copy16_to_lds(p.cs_s + (long long)ri * kDH + 4 * c, dt + wave * 2 * kDH);
@@ -402,89 +530,53 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
       const int e = e_base + t;
       ecol[t] = min(max(p.col[e], 0), cx.Ts - 1);
       ew[t] = (float)p.num[e] / (float)p.den[g0 + lo];
+      einfo[t] = lo | ((int)(e + 1 == estart[lo + 1]) << 8);
     }
   }
-  if (tid < 64) cnt[tid] = tid < nrows ? estart[tid + 1] - estart[tid] : 0;
   __syncthreads();
-  if (tid < 64) {
-    // rank rows by entry count (ties by index): waves then get rows of equal length
-    const int c = cnt[tid];
-    int rank = 0;
-    for (int r = 0; r < 64; ++r) {
-      const int cr = cnt[r];
-      rank += (cr < c) || (cr == c && r < tid);
-    }
-    perm[rank] = tid;
-    if (staged && tid < nrows) {
-      int lmin = INT_MAX, lmax = -1;
-      for (int k = estart[tid] - e_base; k < estart[tid + 1] - e_base; ++k) {
+  if (wave == 0) {  // lane = tile row: sender span of each lane group's rows
+    int lmin = INT_MAX, lmax = -1;
+    if (staged)
+      for (int k = estart[lane] - e_base; k < estart[lane + 1] - e_base; ++k) {
         lmin = min(lmin, ecol[k]);
         lmax = max(lmax, ecol[k]);
       }
-      rfirst[tid] = lmin == INT_MAX ? 0 : lmin;
-      if (lmax - lmin >= kDMax) flag[0] = 1;
+    for (int o = 1; o < RPG; o <<= 1) {
+      lmin = min(lmin, __shfl_xor(lmin, o));
+      lmax = max(lmax, __shfl_xor(lmax, o));
     }
+    gbase[lane] = lmax < 0 ? 0 : lmin;
+    if (unrot && lmax >= 0 && lmax - lmin >= kDMax) flag[0] = 1;
   }
-  __builtin_amdgcn_s_waitcnt(0);  // the U(0..15) table has landed
+  __builtin_amdgcn_s_waitcnt(0);  // the rotation table has landed
   __syncthreads();
   staged = staged && flag[0] == 0;
 
   // ---- build X[64][d_in] ----
-  {
-    const int r = perm[tid >> 3];  // 8 threads per row, rows in entry-count order
-    const int e0 = (tid & 7) * 8;   // features e0..e0+7 and e0+64..e0+71 of every head
-    float rc[8], rs[8];             // U(q_r) at the row's base position
-    if (staged && unrot && r < nrows) {
-      const float* row = cx.cs_s + (long long)rfirst[r] * kDH;
-      const float4 c0 = *reinterpret_cast<const float4*>(row + e0);
-      const float4 c1 = *reinterpret_cast<const float4*>(row + e0 + 4);
-      const float4 s0 = *reinterpret_cast<const float4*>(row + 64 + e0);
-      const float4 s1 = *reinterpret_cast<const float4*>(row + 64 + e0 + 4);
-      rc[0] = c0.x; rc[1] = c0.y; rc[2] = c0.z; rc[3] = c0.w;
-      rc[4] = c1.x; rc[5] = c1.y; rc[6] = c1.z; rc[7] = c1.w;
-      rs[0] = s0.x; rs[1] = s0.y; rs[2] = s0.z; rs[3] = s0.w;
-      rs[4] = s1.x; rs[5] = s1.y; rs[6] = s1.z; rs[7] = s1.w;
+  if (staged) {
+    const int head = wave / WPH;
+    if (head < H) {
+      const GroupLds L{estart, gbase, ecol, ew, einfo, dt, e_base};
+      const int r_first = (wave % WPH) * 8 * RPG + (lane >> 3) * RPG;
+      if (cx.two_tap) {
+        if (unrot) build_groups<true, true, 4>(cx, p, L, head, r_first, RPG, lane, Xs);
+        else build_groups<true, false, 4>(cx, p, L, head, r_first, RPG, lane, Xs);
+      } else {
+        if (unrot) build_groups<false, true, 4>(cx, p, L, head, r_first, RPG, lane, Xs);
+        else build_groups<false, false, 4>(cx, p, L, head, r_first, RPG, lane, Xs);
+      }
     }
-    for (int h0 = 0; h0 < H; h0 += 2) {
-      const int nh = min(2, H - h0);
-      float x[2][16];
+  } else {
+    const int r = tid >> 3;         // 8 threads per row
+    const int e0 = (tid & 7) * 8;   // features e0..e0+7 and e0+64..e0+71 of every head
+    for (int h = 0; h < H; ++h) {
+      float x[16];
 #pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int u = 0; u < 16; ++u) x[hh][u] = 0.0f;
-      if (r < nrows) {
-        if (staged) {
-          const int k0 = estart[r] - e_base, k1 = estart[r + 1] - e_base;
-          const int first = rfirst[r];
-          if (cx.two_tap) {
-            if (unrot) build_row_staged<true, true>(cx, p, k0, k1, ecol, ew, first, dt, h0, nh, e0, x);
-            else build_row_staged<true, false>(cx, p, k0, k1, ecol, ew, first, dt, h0, nh, e0, x);
-          } else {
-            if (unrot) build_row_staged<false, true>(cx, p, k0, k1, ecol, ew, first, dt, h0, nh, e0, x);
-            else build_row_staged<false, false>(cx, p, k0, k1, ecol, ew, first, dt, h0, nh, e0, x);
-          }
-          if (unrot) {  // U(q_r) on each head's sum
-#pragma unroll
-            for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-              for (int u = 0; u < 8; ++u) {
-                const float a = x[hh][u], b = x[hh][u + 8];
-                x[hh][u] = fmaf(a, rc[u], b * rs[u]);
-                x[hh][u + 8] = fmaf(b, rc[u], -a * rs[u]);
-              }
-          }
-        } else {
-          build_row_global(p, cx, g0 + r, h0, e0, x[0]);
-          if (nh > 1) build_row_global(p, cx, g0 + r, h0 + 1, e0, x[1]);
-        }
-      }
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-        if (hh >= nh) break;
-        uint16_t* xr = Xs + r * kXF + (h0 + hh) * kDH;
-        *reinterpret_cast<uint4*>(xr + e0) = pack8(x[hh]);
-        *reinterpret_cast<uint4*>(xr + 64 + e0) = pack8(x[hh] + 8);
-      }
+      for (int u = 0; u < 16; ++u) x[u] = 0.0f;
+      if (r < nrows) build_row_global(p, cx, g0 + r, h, e0, x);
+      uint16_t* xr = Xs + r * kXF + h * kDH;
+      *reinterpret_cast<uint4*>(xr + e0) = pack8(x);
+      *reinterpret_cast<uint4*>(xr + 64 + e0) = pack8(x + 8);
     }
   }
   __syncthreads();
@@ -501,6 +593,7 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   const int lc_store = it.l * 2 + it.c;
   const bf16x8* W = static_cast<const bf16x8*>(p.Wp) + (long long)lc_store * KS * NB * 64 +
                     (4 * head + nt0) * 64 + lane;
+  const int ks0 = (int)(blockIdx.x % (unsigned)H) * (kDH / 16);  // this workgroup's first k-step
 
   f32x16 acc[2][NTW];
 #pragma unroll
@@ -511,16 +604,18 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
       for (int i = 0; i < 16; ++i) acc[mt][q][i] = 0.0f;
 
   bf16x8 wr[4][NTW];  // map fragments of four consecutive k-steps
+  auto kstep = [&](int ks) { int k = ks + ks0; return k >= KS ? k - KS : k; };
   auto load_w = [&](bf16x8* dst, int ks) {
-    const bf16x8* Wk = W + (long long)ks * NB * 64;
+    const bf16x8* Wk = W + (long long)kstep(ks) * NB * 64;
 #pragma unroll
     for (int q = 0; q < NTW; ++q) dst[q] = Wk[q * NTS * 64];
   };
   auto step = [&](bf16x8* wf, int ks) {
+    const int k = kstep(ks);
     bf16x8 xa[2];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
-      xa[mt] = *reinterpret_cast<const bf16x8*>(Xs + (32 * mt + (lane & 31)) * kXF + 16 * ks +
+      xa[mt] = *reinterpret_cast<const bf16x8*>(Xs + (32 * mt + (lane & 31)) * kXF + 16 * k +
                                                 8 * (lane >> 5));
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
@@ -537,19 +632,86 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
     step(wr[2], ks + 2);
     step(wr[3], ks + 3);
   }
-  __syncthreads();  // every wave is done reading X; LDS becomes staging space
+  __syncthreads();  // every wave is done reading X; the X region is free
 
   // ---- store ----
-  uint16_t* stage = Xs + wave * 32 * kXS;
+  const bool rot = it.c == 0 && p.rot;
+  float* rcs = reinterpret_cast<float*>(smem + kOffRcs);
+  float* bias_s = reinterpret_cast<float*>(smem + kOffBias);
+  const int d_r = NB * 32;
+  if (rot) {  // receiver RoPE rows j0..j0+63: 2 per wave instruction; slot c holds chunk
+              // (c & 16) | ((c ^ r) & 15) so that lanes of different rows hit different banks
+    for (int q = wave; q < 32; q += 8) {
+      const int rr = 2 * q + (lane >> 5);
+      const int c = lane & 31;
+      const int cs = (c & 16) | ((c ^ rr) & 15);
+      const int jr = p.pos0_r[it.b] + j0 + min(rr, nrows - 1);
+      copy16_to_lds(p.cs_r + (long long)jr * kDH + 4 * cs, rcs + q * 2 * kDH);
+    }
+  }
+  if (p.bias && wave < d_r / 256)  // 256 floats per wave instruction
+    copy16_to_lds(p.bias + (long long)lc_store * d_r + wave * 256 + 4 * lane, bias_s + wave * 256);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  uint16_t* stage = reinterpret_cast<uint16_t*>(smem + kOffStage) + wave * 32 * kXS;
   uint16_t* dst_head = static_cast<uint16_t*>(p.R) + it.b * p.r_sb + (long long)it.l * p.r_sl +
                        it.c * p.r_sc + head * p.r_sh;
-  const float* bias_head = p.bias ? p.bias + (long long)lc_store * NB * 32 + head * kDH : nullptr;
-  const bool rot = it.c == 0 && p.rot;
-  const float* cr = rot ? p.cs_r + (long long)p.pos0_r[it.b] * kDH : nullptr;
+  const int hi4 = 4 * (lane >> 5);
+  const int mcol = lane & 31;
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
-    epilogue_rows<NTW>(p, acc[mt], feat, bias_head, cr, rot, stage, dst_head, j0 + 32 * mt, Tr,
-                       lane);
+  for (int mt = 0; mt < 2; ++mt) {
+    const int rl = 32 * mt + mcol;  // tile row held by this lane
+    float y[NTW][16];
+#pragma unroll
+    for (int q = 0; q < NTW; ++q)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float4 bv = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (p.bias) bv = *reinterpret_cast<const float4*>(bias_s + head * kDH + feat[q] + 8 * g + hi4);
+        y[q][4 * g + 0] = acc[mt][q][4 * g + 0] + bv.x;
+        y[q][4 * g + 1] = acc[mt][q][4 * g + 1] + bv.y;
+        y[q][4 * g + 2] = acc[mt][q][4 * g + 2] + bv.z;
+        y[q][4 * g + 3] = acc[mt][q][4 * g + 3] + bv.w;
+      }
+    if (rot) {
+      const float4* crow = reinterpret_cast<const float4*>(rcs) + rl * 32;
+#pragma unroll
+      for (int q = 0; q < NTW / 2; ++q)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int c = (feat[q] + 8 * g + hi4) >> 2;  // cos chunk, < 16
+          const float4 cv = crow[(c ^ rl) & 15];
+          const float4 sv = crow[16 | ((c ^ rl) & 15)];
+          const float cc[4] = {cv.x, cv.y, cv.z, cv.w};
+          const float ss[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const float a = y[q][4 * g + u], b = y[q + NTW / 2][4 * g + u];
+            y[q][4 * g + u] = fmaf(a, cc[u], -b * ss[u]);
+            y[q + NTW / 2][4 * g + u] = fmaf(b, cc[u], a * ss[u]);
+          }
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < NTW; ++q)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint2 v = make_uint2(pack2(y[q][4 * g], y[q][4 * g + 1]), pack2(y[q][4 * g + 2], y[q][4 * g + 3]));
+        *reinterpret_cast<uint2*>(stage + mcol * kXS + 32 * q + 8 * g + hi4) = v;
+      }
+    constexpr int LPR = NTW * 4;  // lanes per row, 16 bytes each
+    constexpr int RPP = 64 / LPR;
+#pragma unroll
+    for (int pass = 0; pass < 32 / RPP; ++pass) {
+      const int rr = pass * RPP + lane / LPR;
+      const int ci = lane % LPR;
+      const uint4 v = *reinterpret_cast<const uint4*>(stage + rr * kXS + 8 * ci);
+      const int jj = j0 + 32 * mt + rr;
+      if (jj < Tr)
+        *reinterpret_cast<uint4*>(dst_head + (long long)jj * p.r_st + feat[ci / 4] + 8 * (ci % 4)) = v;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
