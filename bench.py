@@ -176,7 +176,7 @@ def main():
     traffic = kernel_traffic()
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
-            "kernel": "transfer_bf16_kernel", "kernel_ms": round(k_avg, 4),
+            "kernel": "transfer_bf16_tiled_kernel<4>", "kernel_ms": round(k_avg, 4),
             "algorithmic_bytes": bytes_alg,
             "hbm_GBps_algorithmic": round(bytes_alg / (k_avg * 1e-3) / 1e9, 1)}
     cpu = None
