@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <limits.h>
 
+#include <type_traits>
+
 #include "hf_internal.h"
 
 namespace hf {
@@ -312,16 +314,15 @@ static_assert(kSmemBytes <= 160 * 1024, "LDS budget");
 // Group-walk build.  Wave w builds sender head w / WPH for 8 RPG consecutive
 // tile rows (WPH = 8 / RPG waves share a head); lane group g (8 lanes, 16
 // features each) walks the CSR entries of RPG consecutive rows in order, one
-// entry per trip.  An entry whose sender token equals the previous entry's
-// (rows that share a boundary token, forward-filled TA rows) reuses the mixed
-// features already in registers; its loads use an out-of-range buffer offset,
-// which returns zeros without touching memory, so every trip issues the same
-// loads and a ring of R trips keeps R - 1 trips of loads in flight.
+// entry per trip, so a sender token shared by neighbouring rows is read twice
+// in a row (the second read hits the cache).  Trips past a group's last entry
+// use an out-of-range buffer offset, which returns zeros without touching
+// memory, so every trip issues the same loads and a ring of R trips keeps
+// R - 1 trips of loads in flight.
 constexpr int kOOB = (int)0x80000000;  // buffer offset past any slab extent (extents < 2^31)
 
 struct GroupLds {
   const int* estart;  // [65] CSR offsets of the tile rows
-  const int* gbase;   // [64] smallest sender index of each row's group
   const int* ecol;    // staged sender indices
   const float* ew;    // staged weights num / den
   const int* einfo;   // staged row | last-entry-of-row << 8
@@ -332,7 +333,7 @@ struct GroupLds {
 template <bool TWO_TAP>
 struct Trip {
   uint4 a0, a1, b0, b1;  // tap lo / hi: features e0..e0+7 and e0+64..e0+71
-  int code;              // -1: no entry; else row | last << 6 | dup << 7 | (i - base) << 8
+  int code;              // -1: no entry; else row | last << 6 | (i - base) << 8
   float w;
 };
 
@@ -356,7 +357,7 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
 
 template <bool TWO_TAP, bool UNROT, int R>
 __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& p, const GroupLds& L,
-                                             int head, int r_first, int rpg, int lane,
+                                             int base, int head, int r_first, int rpg, int lane,
                                              uint16_t* Xs) {
   const int e0 = (lane & 7) * 8;
   const int kb = L.estart[r_first] - L.e_base;
@@ -364,7 +365,6 @@ __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& 
   int T = 0;  // trips of the wave: the longest group
 #pragma unroll
   for (int g = 0; g < 8; ++g) T = max(T, __builtin_amdgcn_readlane(E, 8 * g));
-  const int base = L.gbase[r_first];
   for (int q = 0; q < rpg; ++q) {  // rows without entries stay zero
     const int r = r_first + q;
     if (L.estart[r + 1] == L.estart[r]) {
@@ -392,37 +392,32 @@ __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& 
   const int hoff = (int)(head * p.s_sh + e0) * 2;  // bytes
   const int tstride = (int)p.s_st * 2;
 
-  int iprev = -1;
   Trip<TWO_TAP> ring[R];
-  float x[16], mp[16];
+  float x[16];
 #pragma unroll
-  for (int u = 0; u < 16; ++u) x[u] = mp[u] = 0.0f;
+  for (int u = 0; u < 16; ++u) x[u] = 0.0f;
 
   auto issue = [&](Trip<TWO_TAP>& t, int k) {
     const bool valid = k < E;
-    int i = iprev, info = 0;
+    int i = 0, info = 0;
     float w = 0.0f;
     if (valid) {
       i = L.ecol[kb + k];
       w = L.ew[kb + k];
       info = L.einfo[kb + k];
     }
-    const bool dup = i == iprev;
-    iprev = i;
-    const int off = dup ? kOOB : hoff + i * tstride;
+    const int off = valid ? hoff + i * tstride : kOOB;
     t.a0 = buf_load16(rlo, off);
     t.a1 = buf_load16(rlo, off + 128);
     if (TWO_TAP) {
       t.b0 = buf_load16(rhi, off);
       t.b1 = buf_load16(rhi, off + 128);
     }
-    t.code = valid ? ((info & 63) | ((info >> 8) << 6) | ((int)dup << 7) | ((UNROT ? i - base : 0) << 8))
-                   : -1;
+    t.code = valid ? ((info & 63) | ((info >> 8) << 6) | ((UNROT ? i - base : 0) << 8)) : -1;
     t.w = w;
   };
   auto consume = [&](const Trip<TWO_TAP>& t) {
     if (t.code < 0) return;
-    const bool dup = (t.code >> 7) & 1;
     const uint32_t l0[4] = {t.a0.x, t.a0.y, t.a0.z, t.a0.w};
     const uint32_t l1[4] = {t.a1.x, t.a1.y, t.a1.z, t.a1.w};
     uint32_t h0[4] = {0, 0, 0, 0}, h1[4] = {0, 0, 0, 0};
@@ -430,30 +425,24 @@ __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& 
       h0[0] = t.b0.x; h0[1] = t.b0.y; h0[2] = t.b0.z; h0[3] = t.b0.w;
       h1[0] = t.b1.x; h1[1] = t.b1.y; h1[2] = t.b1.z; h1[3] = t.b1.w;
     }
+    const float a = t.w * cx.wlo, bq = t.w * cx.whi;  // weight folded into the layer mix
+    float cc[8], ss[8];
+    if (UNROT) table_row(L.dt, t.code >> 8, e0, cc, ss);  // U(p_i - p_base)
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {  // layer mix of this token, or the previous token's
-      float ma = cx.wlo * ((u & 1) ? bf_hi(l0[u >> 1]) : bf_lo(l0[u >> 1]));
-      float mb = cx.wlo * ((u & 1) ? bf_hi(l1[u >> 1]) : bf_lo(l1[u >> 1]));
+    for (int u = 0; u < 8; ++u) {
+      float ma = a * ((u & 1) ? bf_hi(l0[u >> 1]) : bf_lo(l0[u >> 1]));
+      float mb = a * ((u & 1) ? bf_hi(l1[u >> 1]) : bf_lo(l1[u >> 1]));
       if (TWO_TAP) {
-        ma = fmaf(cx.whi, (u & 1) ? bf_hi(h0[u >> 1]) : bf_lo(h0[u >> 1]), ma);
-        mb = fmaf(cx.whi, (u & 1) ? bf_hi(h1[u >> 1]) : bf_lo(h1[u >> 1]), mb);
+        ma = fmaf(bq, (u & 1) ? bf_hi(h0[u >> 1]) : bf_lo(h0[u >> 1]), ma);
+        mb = fmaf(bq, (u & 1) ? bf_hi(h1[u >> 1]) : bf_lo(h1[u >> 1]), mb);
       }
-      mp[u] = dup ? mp[u] : ma;
-      mp[u + 8] = dup ? mp[u + 8] : mb;
-    }
-    const float w = t.w;
-    if (UNROT) {  // x += w U(p_i - p_base) m
-      float cc[8], ss[8];
-      table_row(L.dt, t.code >> 8, e0, cc, ss);
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float ma = w * mp[u], mb = w * mp[u + 8];
+      if (UNROT) {
         x[u] = fmaf(ma, cc[u], fmaf(mb, ss[u], x[u]));
         x[u + 8] = fmaf(mb, cc[u], fmaf(-ma, ss[u], x[u + 8]));
+      } else {
+        x[u] += ma;
+        x[u + 8] += mb;
       }
-    } else {
-#pragma unroll
-      for (int u = 0; u < 16; ++u) x[u] = fmaf(w, mp[u], x[u]);
     }
     if ((t.code >> 6) & 1) {  // last entry of the row: close the rotation, round, store
       if (UNROT) {
@@ -556,14 +545,15 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   if (staged) {
     const int head = wave / WPH;
     if (head < H) {
-      const GroupLds L{estart, gbase, ecol, ew, einfo, dt, e_base};
+      const GroupLds L{estart, ecol, ew, einfo, dt, e_base};
       const int r_first = (wave % WPH) * 8 * RPG + (lane >> 3) * RPG;
+      const int base = gbase[r_first];
       if (cx.two_tap) {
-        if (unrot) build_groups<true, true, 4>(cx, p, L, head, r_first, RPG, lane, Xs);
-        else build_groups<true, false, 4>(cx, p, L, head, r_first, RPG, lane, Xs);
+        if (unrot) build_groups<true, true, 4>(cx, p, L, base, head, r_first, RPG, lane, Xs);
+        else build_groups<true, false, 4>(cx, p, L, base, head, r_first, RPG, lane, Xs);
       } else {
-        if (unrot) build_groups<false, true, 4>(cx, p, L, head, r_first, RPG, lane, Xs);
-        else build_groups<false, false, 4>(cx, p, L, head, r_first, RPG, lane, Xs);
+        if (unrot) build_groups<false, true, 4>(cx, p, L, base, head, r_first, RPG, lane, Xs);
+        else build_groups<false, false, 4>(cx, p, L, base, head, r_first, RPG, lane, Xs);
       }
     }
   } else {
@@ -610,28 +600,44 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
 #pragma unroll
     for (int q = 0; q < NTW; ++q) dst[q] = Wk[q * NTS * 64];
   };
-  auto step = [&](bf16x8* wf, int ks) {
+  auto read_x = [&](bf16x8* xa, int ks) {
     const int k = kstep(ks);
-    bf16x8 xa[2];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
       xa[mt] = *reinterpret_cast<const bf16x8*>(Xs + (32 * mt + (lane & 31)) * kXF + 16 * k +
                                                 8 * (lane >> 5));
+  };
+  bf16x8 xc[2], xn[2];  // X fragments of this k-step and the next
+  // One k-step: read next X from LDS, multiply, then refill this map slot with
+  // k-step ks + 4.  LOAD is a constant so that the loop body has no branches
+  // and every wait on a map fragment keeps the three younger k-steps in flight.
+  auto step = [&](bf16x8* wf, int ks, auto load) {
+    read_x(xn, ks + 1);
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int q = 0; q < NTW; ++q)
-        acc[mt][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[q], xa[mt], acc[mt][q], 0, 0, 0);
-    if (ks + 4 < KS) load_w(wf, ks + 4);
+        acc[mt][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[q], xc[mt], acc[mt][q], 0, 0, 0);
+    if (decltype(load)::value) load_w(wf, ks + 4);
+    xc[0] = xn[0];
+    xc[1] = xn[1];
+    __builtin_amdgcn_sched_barrier(0);  // keep the refill in this k-step
   };
+  using Load = std::true_type;
+  using NoLoad = std::false_type;
 #pragma unroll
   for (int u = 0; u < 4; ++u) load_w(wr[u], u);  // KS is a multiple of 8
-  for (int ks = 0; ks < KS; ks += 4) {
-    step(wr[0], ks);
-    step(wr[1], ks + 1);
-    step(wr[2], ks + 2);
-    step(wr[3], ks + 3);
+  read_x(xc, 0);
+  for (int ks = 0; ks < KS - 4; ks += 4) {
+    step(wr[0], ks, Load());
+    step(wr[1], ks + 1, Load());
+    step(wr[2], ks + 2, Load());
+    step(wr[3], ks + 3, Load());
   }
+  step(wr[0], KS - 4, NoLoad());
+  step(wr[1], KS - 3, NoLoad());
+  step(wr[2], KS - 2, NoLoad());
+  step(wr[3], KS - 1, NoLoad());
   __syncthreads();  // every wave is done reading X; the X region is free
 
   // ---- store ----
