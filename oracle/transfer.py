@@ -141,3 +141,103 @@ def transfer_rows(get_sender, layer_table, csr, A_lc, b_lc, rope, d_h,
             y = _rope.rotate(y[:, None, :], [qpos], rope["theta_r"])[:, 0, :]
         out[:, n, :] = y
     return (out, xs) if return_features else out
+
+
+# ---------------------------------------------------------------------------
+# Concatenated-feature maps (the paper's own layer alignment, Sec. 3.1 Eq. 2).
+#
+# Receiver layer l reads n sender layers taps[l] = (t_1, .., t_n) -- for the
+# paper's map the three layers of Eq. 1 -- without interpolation.  For each
+# tap t the aligned feature is
+#     x_j^t = sum over the CSR row of (num / den_j) * U_s(p_i) S[t, c, :, i, :]
+# (un-rotation for post-RoPE keys only), flattened head-major, and the map
+# sees their concatenation x_j = [x_j^{t_1} | .. | x_j^{t_n}] (Eq. 2), so
+# A[l, c] is [d_R, n * d_S].  The rest (bias, receiver RoPE, reshape) is as
+# in ``transfer``.
+# ---------------------------------------------------------------------------
+
+def aligned_layer(S, sender_layer, csr, rope, role):
+    """x^t of one sender layer t, fp64 [T_R, H_S * d_h]."""
+    S = np.asarray(S, dtype=np.float64)
+    _, _, H_s, T_s, d_h = S.shape
+    m = S[sender_layer, role]
+    if role == K and rope is not None and rope.get("unrotate_sender_k", False):
+        m = _rope.unrotate(m, rope.get("pos0_s", 0) + np.arange(T_s), rope["theta_s"])
+    u = m.transpose(1, 0, 2).reshape(T_s, H_s * d_h)                    # head-major
+    return _weights_matrix(csr, T_s) @ u
+
+
+def features_taps(S, taps, csr, rope, layer, role):
+    """Concatenated features of Eq. 2, fp64 [T_R, n * H_S * d_h]."""
+    return np.concatenate([aligned_layer(S, int(t), csr, rope, role)
+                           for t in np.asarray(taps)[layer]], axis=1)
+
+
+def transfer_taps(S, taps, csr, A, b=None, rope=None, H_r=None):
+    """Whole receiver cache with concatenated-feature maps.
+
+    taps  int [L_R, n] sender layers of each receiver layer
+    A     [L_R, 2, d_R, n * d_S];  b  [L_R, 2, d_R] or None
+    other arguments and the result as in ``transfer``
+    """
+    S = np.asarray(S, dtype=np.float64)
+    A = np.asarray(A, dtype=np.float64)
+    taps = np.asarray(taps)
+    _, _, H_s, _, d_h = S.shape
+    L_r, _, d_r, d_in = A.shape
+    if d_in != taps.shape[1] * H_s * d_h:
+        raise ValueError("A's input size must be n_taps * H_S * d_h")
+    H_r = d_r // d_h if H_r is None else H_r
+    T_r = np.asarray(csr[0]).size - 1
+    out = np.empty((L_r, 2, H_r, T_r, d_h), dtype=np.float64)
+    for l in range(L_r):
+        for c in (K, V):
+            y = features_taps(S, taps, csr, rope, l, c) @ A[l, c].T
+            if b is not None:
+                y = y + np.asarray(b, dtype=np.float64)[l, c][None, :]
+            y = y.reshape(T_r, H_r, d_h).transpose(1, 0, 2)
+            if c == K and rope is not None and rope.get("rotate_receiver_k", False):
+                y = _rope.rotate(y, rope.get("pos0_r", 0) + np.arange(T_r), rope["theta_r"])
+            out[l, c] = y
+    return out
+
+
+def transfer_rows_taps(get_sender, taps, csr, A_lc, b_lc, rope, d_h, layer, role, rows,
+                       return_features=False):
+    """Selected receiver rows of one (layer, role) with concatenated-feature
+    maps, entry by entry (get_sender as in ``transfer_rows``)."""
+    taps = np.asarray(taps)[layer]
+    row_ptr, col, num, den = (np.asarray(t, dtype=np.int64) for t in csr)
+    A_lc = np.asarray(A_lc, dtype=np.float64)
+    d_r, d_in = A_lc.shape
+    H_r = d_r // d_h
+    rows = np.asarray(rows, dtype=np.int64)
+    out = np.empty((H_r, rows.size, d_h), dtype=np.float64)
+    xs = np.empty((rows.size, d_in), dtype=np.float64)
+    unrot = role == K and rope is not None and rope.get("unrotate_sender_k", False)
+    rot = role == K and rope is not None and rope.get("rotate_receiver_k", False)
+    for n, j in enumerate(rows):
+        ents = range(row_ptr[j], row_ptr[j + 1])
+        idx = np.asarray([col[e] for e in ents], dtype=np.int64)
+        blocks = []
+        for t in taps:
+            St = get_sender(int(t), role, idx)                           # [H_S, len, d_h]
+            x = np.zeros(St.shape[0] * d_h, dtype=np.float64)
+            for q, e in enumerate(ents):
+                m = St[:, q, :]
+                if unrot:
+                    p = rope.get("pos0_s", 0) + int(col[e])
+                    m = _rope.unrotate(m[:, None, :], [p], rope["theta_s"])[:, 0, :]
+                x += (float(num[e]) / float(den[j])) * m.reshape(-1)
+            blocks.append(x)
+        x = np.concatenate(blocks)
+        xs[n] = x
+        y = A_lc @ x
+        if b_lc is not None:
+            y = y + np.asarray(b_lc, dtype=np.float64)
+        y = y.reshape(H_r, d_h)
+        if rot:
+            qpos = rope.get("pos0_r", 0) + int(j)
+            y = _rope.rotate(y[:, None, :], [qpos], rope["theta_r"])[:, 0, :]
+        out[:, n, :] = y
+    return (out, xs) if return_features else out
