@@ -40,31 +40,46 @@ def log(*a):
 
 
 def algorithmic_cost(cfg, seg):
-    """Flops and HBM bytes of one transfer kernel launch (see DESIGN.md):
-    flops = 2 roles x L_r x 2 d_in d_r per receiver token; bytes = each sender
+    """Flops and HBM bytes of one transfer kernel launch:
+    flops = 2 roles x L_r x 2 n d_r per receiver token, n the map's input size
+    (d_in, or 3 d_in for the three-layer neighbourhood); bytes = each sender
     layer the layer map uses read once per role, the receiver cache written
     once, the maps read once."""
     from paper_2609_32259_amd import heterofold as hf
     T_r = int(seg.r_len.sum())
     T_s = int(seg.s_len.sum())
     el = 2 if cfg.dtype == "bf16" else 4
-    flops = 2 * cfg.L_r * 2 * cfg.d_in * cfg.d_r * T_r
-    lo, hi, rem, _ = hf.hf_build_layer_map(cfg.L_s, cfg.L_r)
-    used = set(lo.tolist()) | {int(h) for h, r in zip(hi, rem) if r}
+    n = cfg.d_map_in
+    flops = 2 * cfg.L_r * 2 * n * cfg.d_r * T_r
+    if cfg.layer_map == "neighbor3":
+        used = set(hf.hf_build_layer_taps(cfg.L_s, cfg.L_r).reshape(-1).tolist())
+    else:
+        lo, hi, rem, _ = hf.hf_build_layer_map(cfg.L_s, cfg.L_r)
+        used = set(lo.tolist()) | {int(h) for h, r in zip(hi, rem) if r}
     read = len(used) * 2 * T_s * cfg.d_in * el
     write = cfg.L_r * 2 * T_r * cfg.d_r * el
-    maps = cfg.L_r * 2 * cfg.d_r * cfg.d_in * el + cfg.L_r * 2 * cfg.d_r * 4
+    maps = cfg.L_r * 2 * cfg.d_r * n * el + cfg.L_r * 2 * cfg.d_r * 4
     return flops, read + write + maps
 
 
-def kernel_traffic():
+def kernel_name(cfg):
+    """The transfer kernel hf_transfer_kv(_taps) launches for this shape."""
+    if cfg.dtype != "bf16":
+        return "transfer_f32_kernel"
+    if cfg.H_r in (4, 8) and cfg.H_s <= 8:
+        return f"transfer_bf16_tiled_kernel<{cfg.H_r // 2}, {'true' if cfg.n_taps > 1 else 'false'}>"
+    return f"transfer_bf16_direct_kernel<{cfg.H_r}>"
+
+
+def kernel_traffic(cfg):
     """HBM bytes per transfer launch from the committed rocprofv3 counter
-    summary, or None if there is none or the kernel source changed since."""
+    summary, or None if there is none for this workload or the kernel source
+    changed since."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
         src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
-        if rec.get("kernel_source_sha256") != src:
+        if rec.get("kernel_source_sha256") != src or rec.get("workload_name") != cfg.name:
             return None
         return rec.get("bytes_per_launch")
     except (OSError, ValueError):
@@ -86,20 +101,27 @@ def cpu_baseline(wl, budget_s=30.0):
     t0 = time.perf_counter()
     csr = [al.build_alignment(*seg.seq(b), "overlap") for b in range(seg.batch)]
     t_align = time.perf_counter() - t0
-    lt = lm.interp2(cfg.L_s, cfg.L_r)
     layer = 1 if cfg.L_r > 1 else 0
-    lo, hi = int(lt[0][layer]), int(lt[1][layer])
-    sub = (np.array([0]), np.array([1 if hi != lo else 0]), lt[2][layer:layer + 1], lt[3][layer:layer + 1])
     t_layer = 0.0
     for b in range(seg.batch):
         T_s = int(seg.s_len[b])
-        taps = [lo] if hi == lo else [lo, hi]
-        S = wl.S[b, taps, :, :, :T_s, :].float().cpu().numpy().astype(np.float64)
         A = wl.A[layer:layer + 1].float().cpu().numpy().astype(np.float64)
         bias = wl.bias[layer:layer + 1].float().cpu().numpy().astype(np.float64)
         rp = None if wl.rope is None else dict(wl.rope, pos0_s=0, pos0_r=0)
-        t0 = time.perf_counter()
-        tr.transfer(S, sub, csr[b], A, bias, rp, H_r=cfg.H_r)
+        if cfg.layer_map == "neighbor3":
+            taps = lm.neighbor3(cfg.L_s, cfg.L_r)[layer]
+            S = wl.S[b, list(taps), :, :, :T_s, :].float().cpu().numpy().astype(np.float64)
+            t0 = time.perf_counter()
+            tr.transfer_taps(S, np.arange(len(taps))[None, :], csr[b], A, bias, rp, H_r=cfg.H_r)
+        else:
+            lt = lm.interp2(cfg.L_s, cfg.L_r)
+            lo, hi = int(lt[0][layer]), int(lt[1][layer])
+            sub = (np.array([0]), np.array([1 if hi != lo else 0]), lt[2][layer:layer + 1],
+                   lt[3][layer:layer + 1])
+            taps = [lo] if hi == lo else [lo, hi]
+            S = wl.S[b, taps, :, :, :T_s, :].float().cpu().numpy().astype(np.float64)
+            t0 = time.perf_counter()
+            tr.transfer(S, sub, csr[b], A, bias, rp, H_r=cfg.H_r)
         t_layer += time.perf_counter() - t0
         del S
     est = t_align + cfg.L_r * t_layer
@@ -145,7 +167,8 @@ def main():
     cfg = synth.CONFIGS[args.workload]
     log(f"[bench] workload {cfg.name}: generating inputs on the GPU")
     wl = synth.make_workload(cfg, seed=args.seed, device="cuda")
-    path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r)
+    path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r,
+                        layer_map=cfg.layer_map)
     torch.cuda.synchronize()
     T_r = int(wl.seg.r_len.sum())
     T_s = int(wl.seg.s_len.sum())
@@ -168,15 +191,21 @@ def main():
     a_ms, a_n = hf.hf_profiler_query(hf.HF_KERNEL_ALIGNMENT)
     r_ms, r_n = hf.hf_profiler_query(hf.HF_KERNEL_ROPE_TABLES)
     k_avg = k_ms / max(k_n, 1)
-    log(f"[bench] step {ms_step:.3f} ms; transfer kernel {k_avg:.3f} ms x{k_n}; "
-        f"alignment {a_ms / max(a_n, 1):.3f} ms; rope tables {r_ms / max(r_n, 1):.3f} ms")
+    ks = hf.hf_profiler_samples(hf.HF_KERNEL_TRANSFER).astype(np.float64)
+    k_med, k_min, k_p90 = (float(np.median(ks)), float(ks.min()), float(np.percentile(ks, 90)))
+    log(f"[bench] step {ms_step:.3f} ms; transfer kernel mean {k_avg:.3f} ms, median {k_med:.3f}, "
+        f"min {k_min:.3f}, p90 {k_p90:.3f} (x{k_n}); alignment {a_ms / max(a_n, 1):.3f} ms; "
+        f"rope tables {r_ms / max(r_n, 1):.3f} ms")
 
     flops, bytes_alg = algorithmic_cost(cfg, wl.seg)
     achieved = flops / (k_avg * 1e-3) / 1e12
-    traffic = kernel_traffic()
+    traffic = kernel_traffic(cfg)
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
-            "kernel": "transfer_bf16_tiled_kernel<4>", "kernel_ms": round(k_avg, 4),
+            "kernel": kernel_name(cfg), "kernel_ms": round(k_avg, 4),
+            "kernel_ms_median": round(k_med, 4), "kernel_ms_min": round(k_min, 4),
+            "kernel_ms_p90": round(k_p90, 4),
+            "alignment_ms": round(a_ms / max(a_n, 1), 4),
             "algorithmic_bytes": bytes_alg,
             "hbm_GBps_algorithmic": round(bytes_alg / (k_avg * 1e-3) / 1e9, 1)}
     cpu = None
@@ -199,7 +228,7 @@ def main():
         "config": {"workload": cfg.name, "batch": wl.seg.batch, "T_s": T_s, "T_r": T_r,
                    "L_s": cfg.L_s, "L_r": cfg.L_r, "H_s": cfg.H_s, "H_r": cfg.H_r, "d_h": cfg.d_h,
                    "rope": list(cfg.rope) if cfg.rope else None, "alignment": "overlap",
-                   "layer_map": "interp2", "parallelism": "single-gpu"},
+                   "layer_map": cfg.layer_map, "parallelism": "single-gpu"},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -9,7 +9,8 @@
  *   1. hf_build_alignment  -- which sender tokens each receiver token reads,
  *      from the two tokenizers' character spans (Sec. 3.1 "Token Alignment";
  *      App. B.1), as a CSR span table.
- *   2. hf_build_layer_map  -- which sender layers feed each receiver layer.
+ *   2. hf_build_layer_map  -- which sender layers feed each receiver layer
+ *      (hf_build_layer_taps: the paper's three-layer neighbourhood).
  *   3. hf_transfer_kv      -- gather, segment-mean and layer-interpolate the
  *      sender cache, un-rotate post-RoPE sender keys, apply the folded affine
  *      map y = A x + b of each receiver layer and role (Eq. 9), rotate keys at
@@ -146,6 +147,17 @@ int32_t hf_validate_offsets_host(int32_t T, const int32_t* beg, const int32_t* e
 int32_t hf_build_layer_map(int32_t L_s, int32_t L_r, int32_t mode, int32_t* lo, int32_t* hi,
                            int32_t* rem, int32_t* den);
 
+/*
+ * The paper's own layer alignment (Sec. 3.1 "Layer Alignment", Eq. 1),
+ * 0-based: receiver layer j is matched to sender layer
+ * pi(j) = round(j (L_s-1)/(L_r-1)) (exact rational, ties to even; L_r == 1
+ * gives 0) and reads the three sender layers clip(pi-4, pi, pi+4) to
+ * [0, L_s-1].  taps: host int32 [L_r][3], caller-owned.  Pure host code.
+ * Feed the table to hf_transfer_kv_taps with n_taps = 3.
+ * Errors: HF_ERR_SHAPE (L_s < 1 or L_r < 1), HF_ERR_NULL.
+ */
+int32_t hf_build_layer_taps(int32_t L_s, int32_t L_r, int32_t* taps);
+
 /* ------------------------------------------------------------------------ */
 /* Step 3: KV transfer.                                                      */
 /* ------------------------------------------------------------------------ */
@@ -238,6 +250,29 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
                        const hf_rope* rope, void* workspace, size_t workspace_bytes,
                        void* stream);
 
+/*
+ * hf_transfer_kv for maps over concatenated sender layers (Sec. 3.1 Eq. 2,
+ * with the folded map of Eq. 9): receiver layer l reads the n_taps sender
+ * layers taps[l][0..n_taps) without interpolation, and its map sees their
+ * aligned features side by side,
+ *   x_j = [x_j^{t_1} | ... | x_j^{t_n}],
+ *   x_j^t = sum over row j of (num/den_j) U_s(pos0_s + i) S[t, c, :, i, :]
+ * (each block flattened head-major; U_s for keys when unrotate_sender_k).
+ * Arguments as hf_transfer_kv, except
+ *   n_taps     1..3 (3 for hf_build_layer_taps's table)
+ *   taps       host int32 [receiver->L][n_taps], sender layers in [0, sender->L)
+ *   A_packed   maps A[l, c] of shape [d_r][n_taps * d_in] packed by
+ *              hf_pack_maps with its d_in argument = n_taps * sender->H * d_h.
+ * Shapes supported, numerics, ownership and errors as hf_transfer_kv; for
+ * HF_F32 the limit is n_taps * d_in <= 4096.
+ */
+int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                            const int32_t* row_ptr, const int32_t* col, const int32_t* num,
+                            const int32_t* den, int32_t n_taps, const int32_t* taps,
+                            const hf_kv_desc* sender, const hf_kv_desc* receiver,
+                            const void* A_packed, const float* bias, const hf_rope* rope,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Kernel timing (tracing).                                                  */
 /* ------------------------------------------------------------------------ */
@@ -259,6 +294,13 @@ typedef enum {
 int32_t hf_profiler_enable(int32_t on);
 int32_t hf_profiler_reset(void);
 int32_t hf_profiler_query(int32_t kernel_id, double* total_ms, int64_t* launches);
+/*
+ * Per-launch durations (ms) of one kernel since the last reset, oldest
+ * first: the first min(capacity, count) of them are copied to ms (host,
+ * caller-owned; the profiler keeps at most 4096 per kernel) and *count gets
+ * how many it keeps.  Waits for the recorded events like hf_profiler_query.
+ */
+int32_t hf_profiler_samples(int32_t kernel_id, float* ms, int64_t capacity, int64_t* count);
 
 #ifdef __cplusplus
 }

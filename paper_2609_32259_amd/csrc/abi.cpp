@@ -51,7 +51,10 @@ struct Profiler {
   std::vector<EventPair> pending;
   double total_ms[HF_KERNEL_COUNT] = {};
   int64_t launches[HF_KERNEL_COUNT] = {};
+  std::vector<float> samples[HF_KERNEL_COUNT];  // per-launch ms, at most kMaxSamples each
 };
+
+constexpr size_t kMaxSamples = 4096;
 
 Profiler& prof() {
   static Profiler p;
@@ -112,6 +115,7 @@ int32_t drain_profiler(Profiler& p) {
     }
     p.total_ms[e.kernel] += ms;
     p.launches[e.kernel] += 1;
+    if (p.samples[e.kernel].size() < kMaxSamples) p.samples[e.kernel].push_back(ms);
   }
   p.pending.clear();
   return HF_OK;
@@ -276,6 +280,26 @@ int32_t hf_build_layer_map(int32_t L_s, int32_t L_r, int32_t mode, int32_t* lo, 
   return ok();
 }
 
+int32_t hf_build_layer_taps(int32_t L_s, int32_t L_r, int32_t* taps) {
+  if (L_s < 1 || L_r < 1) return fail(HF_ERR_SHAPE, "layer counts must be >= 1");
+  if (!taps) return fail(HF_ERR_NULL, "output table is NULL");
+  for (int32_t j = 0; j < L_r; ++j) {
+    // pi = round(j (L_s-1) / (L_r-1)), ties to even, on exact integers
+    int64_t pi = 0;
+    if (L_r > 1) {
+      const int64_t n = (int64_t)j * (L_s - 1), d = L_r - 1;
+      pi = n / d;
+      const int64_t r2 = 2 * (n % d);
+      if (r2 > d || (r2 == d && (pi & 1))) ++pi;
+    }
+    for (int t = 0; t < 3; ++t) {
+      const int64_t v = pi + 4 * (t - 1);
+      taps[3 * j + t] = (int32_t)std::min<int64_t>(std::max<int64_t>(v, 0), L_s - 1);
+    }
+  }
+  return ok();
+}
+
 size_t hf_packed_maps_bytes(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype) {
   if (L_r < 1 || d_r < 1 || d_in < 1) return 0;
   const size_t el = dtype == HF_BF16 ? 2 : (dtype == HF_F32 ? 4 : 0);
@@ -344,16 +368,34 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
   return rope_bytes(rs.P_s, sender->d_h) + rope_bytes(rs.P_r, receiver->d_h);
 }
 
-int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
-                       const int32_t* row_ptr, const int32_t* col, const int32_t* num,
-                       const int32_t* den, const int32_t* lo, const int32_t* hi,
-                       const int32_t* rem, const int32_t* den_l, const hf_kv_desc* sender,
-                       const hf_kv_desc* receiver, const void* A_packed, const float* bias,
-                       const hf_rope* rope, void* workspace, size_t workspace_bytes,
-                       void* stream) {
+namespace {
+
+// Which sender layers feed each receiver layer: an interpolation table
+// (lo, hi, rem, den) or n_taps concatenated layers.
+struct LayerSpec {
+  bool concat = false;
+  int32_t n_taps = 1;
+  const int32_t* lo = nullptr;
+  const int32_t* hi = nullptr;
+  const int32_t* rem = nullptr;
+  const int32_t* den_l = nullptr;
+  const int32_t* taps = nullptr;  // [L_r][n_taps]
+};
+
+int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                      const int32_t* row_ptr, const int32_t* col, const int32_t* num,
+                      const int32_t* den, const LayerSpec& ls, const hf_kv_desc* sender,
+                      const hf_kv_desc* receiver, const void* A_packed, const float* bias,
+                      const hf_rope* rope, void* workspace, size_t workspace_bytes,
+                      void* stream) {
   if (B < 1 || B > HF_MAX_BATCH) return fail(HF_ERR_SHAPE, "B=%d outside [1, %d]", B, HF_MAX_BATCH);
   if (!s_len || !r_len) return fail(HF_ERR_NULL, "s_len / r_len is NULL");
-  if (!lo || !hi || !rem || !den_l) return fail(HF_ERR_NULL, "layer table is NULL");
+  if (ls.concat) {
+    if (!ls.taps) return fail(HF_ERR_NULL, "layer taps table is NULL");
+    if (ls.n_taps < 1 || ls.n_taps > 3) return fail(HF_ERR_SHAPE, "n_taps %d outside [1, 3]", ls.n_taps);
+  } else if (!ls.lo || !ls.hi || !ls.rem || !ls.den_l) {
+    return fail(HF_ERR_NULL, "layer table is NULL");
+  }
   if (!row_ptr || !col || !num || !den) return fail(HF_ERR_NULL, "alignment table is NULL");
   if (!A_packed) return fail(HF_ERR_NULL, "A_packed is NULL");
   int32_t st;
@@ -366,14 +408,15 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
   if (L_s > 256) return fail(HF_ERR_SHAPE, "sender layers %d > 256", L_s);
   if (!aligned16(A_packed)) return fail(HF_ERR_SHAPE, "A_packed not 16-byte aligned");
   if (bias && (reinterpret_cast<uintptr_t>(bias) & 15u)) return fail(HF_ERR_SHAPE, "bias not 16-byte aligned");
-  const int d_in = sender->H * d_h;
+  const int d_in = sender->H * d_h;   // one tap
+  const int d_all = ls.n_taps * d_in;  // the map's input size
   if (dtype == HF_BF16) {
     if (d_h != 128) return fail(HF_ERR_UNSUPPORTED, "bf16 path needs d_h == 128 (got %d)", d_h);
     const int H = receiver->H;
     if (H != 2 && H != 4 && H != 8)
       return fail(HF_ERR_UNSUPPORTED, "bf16 path needs receiver H in {2,4,8} (got %d)", H);
-  } else if (d_in > 4096 || d_in % 4) {
-    return fail(HF_ERR_UNSUPPORTED, "fp32 path needs d_in <= 4096 and d_in %% 4 == 0");
+  } else if (d_all > 4096 || d_in % 4) {
+    return fail(HF_ERR_UNSUPPORTED, "fp32 path needs n_taps*d_in <= 4096 and d_in %% 4 == 0");
   }
   int64_t sum_r = 0;
   for (int b = 0; b < B; ++b) {
@@ -386,9 +429,17 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
   }
   if (sum_r > INT32_MAX) return fail(HF_ERR_SHAPE, "too many receiver tokens");
   for (int j = 0; j < L_r; ++j) {
-    if (lo[j] < 0 || lo[j] >= L_s || hi[j] < 0 || hi[j] >= L_s)
+    if (ls.concat) {
+      for (int t = 0; t < ls.n_taps; ++t) {
+        const int32_t v = ls.taps[(int64_t)j * ls.n_taps + t];
+        if (v < 0 || v >= L_s)
+          return fail(HF_ERR_SHAPE, "taps row %d names a sender layer outside [0, %d)", j, L_s);
+      }
+      continue;
+    }
+    if (ls.lo[j] < 0 || ls.lo[j] >= L_s || ls.hi[j] < 0 || ls.hi[j] >= L_s)
       return fail(HF_ERR_SHAPE, "layer table row %d names a sender layer outside [0, %d)", j, L_s);
-    if (den_l[j] < 1 || rem[j] < 0 || rem[j] >= den_l[j])
+    if (ls.den_l[j] < 1 || ls.rem[j] < 0 || ls.rem[j] >= ls.den_l[j])
       return fail(HF_ERR_SHAPE, "layer table row %d needs 0 <= rem < den", j);
   }
   if (rope && (!(rope->theta_s > 0) || !(rope->theta_r > 0) || !std::isfinite(rope->theta_s) ||
@@ -424,7 +475,9 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
   a.H_r = receiver->H;
   a.d_h = d_h;
   a.B = B;
-  a.rows_per_tile = hf::transfer_rows_per_tile(dtype, receiver->H, d_in);
+  a.n_taps = ls.n_taps;
+  a.concat = ls.concat ? 1 : 0;
+  a.rows_per_tile = hf::transfer_rows_per_tile(dtype, receiver->H, sender->H, ls.n_taps, d_h);
   int tiles = 0, row0 = 0;
   for (int b = 0; b < B; ++b) {
     a.tile_start[b] = tiles;
@@ -447,10 +500,18 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
   a.tiles_per_lc = tiles;
   if ((int64_t)tiles * L_r * 2 > INT32_MAX) return fail(HF_ERR_SHAPE, "too many work items");
   for (int j = 0; j < L_r; ++j) {
-    a.lo[j] = (uint8_t)lo[j];
-    a.hi[j] = (uint8_t)hi[j];
-    a.wlo[j] = (float)((double)(den_l[j] - rem[j]) / (double)den_l[j]);
-    a.whi[j] = (float)((double)rem[j] / (double)den_l[j]);
+    if (ls.concat) {  // each tap is one sender layer with weight 1
+      for (int t = 0; t < ls.n_taps; ++t) a.taps[j][t] = (uint8_t)ls.taps[(int64_t)j * ls.n_taps + t];
+      a.lo[j] = a.hi[j] = a.taps[j][0];
+      a.wlo[j] = 1.0f;
+      a.whi[j] = 0.0f;
+      continue;
+    }
+    a.lo[j] = (uint8_t)ls.lo[j];
+    a.hi[j] = (uint8_t)ls.hi[j];
+    a.taps[j][0] = a.lo[j];
+    a.wlo[j] = (float)((double)(ls.den_l[j] - ls.rem[j]) / (double)ls.den_l[j]);
+    a.whi[j] = (float)((double)ls.rem[j] / (double)ls.den_l[j]);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* w = static_cast<char*>(workspace);
@@ -479,6 +540,38 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
   return ok();
 }
 
+}  // namespace
+
+int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                       const int32_t* row_ptr, const int32_t* col, const int32_t* num,
+                       const int32_t* den, const int32_t* lo, const int32_t* hi,
+                       const int32_t* rem, const int32_t* den_l, const hf_kv_desc* sender,
+                       const hf_kv_desc* receiver, const void* A_packed, const float* bias,
+                       const hf_rope* rope, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  LayerSpec ls;
+  ls.lo = lo;
+  ls.hi = hi;
+  ls.rem = rem;
+  ls.den_l = den_l;
+  return transfer_impl(B, s_len, r_len, row_ptr, col, num, den, ls, sender, receiver, A_packed,
+                       bias, rope, workspace, workspace_bytes, stream);
+}
+
+int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                            const int32_t* row_ptr, const int32_t* col, const int32_t* num,
+                            const int32_t* den, int32_t n_taps, const int32_t* taps,
+                            const hf_kv_desc* sender, const hf_kv_desc* receiver,
+                            const void* A_packed, const float* bias, const hf_rope* rope,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  LayerSpec ls;
+  ls.concat = true;
+  ls.n_taps = n_taps;
+  ls.taps = taps;
+  return transfer_impl(B, s_len, r_len, row_ptr, col, num, den, ls, sender, receiver, A_packed,
+                       bias, rope, workspace, workspace_bytes, stream);
+}
+
 int32_t hf_profiler_enable(int32_t on) {
   Profiler& p = prof();
   std::lock_guard<std::mutex> g(p.mu);
@@ -493,6 +586,7 @@ int32_t hf_profiler_reset(void) {
   for (int k = 0; k < HF_KERNEL_COUNT; ++k) {
     p.total_ms[k] = 0.0;
     p.launches[k] = 0;
+    p.samples[k].clear();
   }
   return st == HF_OK ? ok() : st;
 }
@@ -506,6 +600,20 @@ int32_t hf_profiler_query(int32_t kernel_id, double* total_ms, int64_t* launches
   if (st != HF_OK) return st;
   *total_ms = p.total_ms[kernel_id];
   *launches = p.launches[kernel_id];
+  return ok();
+}
+
+int32_t hf_profiler_samples(int32_t kernel_id, float* ms, int64_t capacity, int64_t* count) {
+  if (kernel_id < 0 || kernel_id >= HF_KERNEL_COUNT) return fail(HF_ERR_SHAPE, "kernel id %d unknown", kernel_id);
+  if (!count || (capacity > 0 && !ms)) return fail(HF_ERR_NULL, "output pointer is NULL");
+  Profiler& p = prof();
+  std::lock_guard<std::mutex> g(p.mu);
+  const int32_t st = drain_profiler(p);
+  if (st != HF_OK) return st;
+  const std::vector<float>& v = p.samples[kernel_id];
+  const int64_t n = std::min<int64_t>(capacity, (int64_t)v.size());
+  for (int64_t k = 0; k < n; ++k) ms[k] = v[k];
+  *count = (int64_t)v.size();
   return ok();
 }
 

@@ -67,14 +67,17 @@ struct TransferArgs {
   int32_t row0[HF_MAX_BATCH];    // first CSR row of each sequence
   int32_t pos0_s[HF_MAX_BATCH];
   int32_t pos0_r[HF_MAX_BATCH];
+  int32_t n_taps;           // sender layers per receiver layer whose features are concatenated
+  int32_t concat;           // 1: taps[l][0..n_taps) each with weight 1; 0: interpolate lo, hi
   uint8_t lo[HF_MAX_LAYERS];
   uint8_t hi[HF_MAX_LAYERS];
+  uint8_t taps[HF_MAX_LAYERS][3];
   float wlo[HF_MAX_LAYERS];
   float whi[HF_MAX_LAYERS];
 };
 
 // Rows per workgroup tile of the transfer kernels.
-int transfer_rows_per_tile(int dtype, int H_r, int d_in);
+int transfer_rows_per_tile(int dtype, int H_r, int H_s, int n_taps, int d_h);
 
 hipError_t launch_alignment(const AlignArgs& a, hipStream_t s);
 hipError_t launch_rope_table(float* tab, int P, int d_h, double theta, hipStream_t s);

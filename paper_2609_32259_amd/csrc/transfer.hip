@@ -127,14 +127,17 @@ struct Ctx {
   int Ts;
 };
 
-__device__ __forceinline__ Ctx make_ctx(const TransferArgs& p, const Item& it) {
+// Tap t of the layer map: with concatenated taps, sender layer taps[l][t]
+// with weight 1; otherwise (t = 0) the interpolation of lo and hi.
+__device__ __forceinline__ Ctx make_ctx(const TransferArgs& p, const Item& it, int t = 0) {
   Ctx x;
   const uint16_t* Sb = static_cast<const uint16_t*>(p.S) + it.b * p.s_sb + it.c * p.s_sc;
-  x.S_lo = Sb + (long long)p.lo[it.l] * p.s_sl;
-  x.S_hi = Sb + (long long)p.hi[it.l] * p.s_sl;
+  const int lo = p.concat ? p.taps[it.l][t] : p.lo[it.l];
+  x.S_lo = Sb + (long long)lo * p.s_sl;
+  x.S_hi = Sb + (long long)(p.concat ? lo : p.hi[it.l]) * p.s_sl;
   x.cs_s = (it.c == 0 && p.unrot) ? p.cs_s + (long long)p.pos0_s[it.b] * kDH : nullptr;
-  x.wlo = p.wlo[it.l];
-  x.whi = p.whi[it.l];
+  x.wlo = p.concat ? 1.0f : p.wlo[it.l];
+  x.whi = p.concat ? 0.0f : p.whi[it.l];
   x.two_tap = x.whi != 0.0f;
   x.Ts = p.Ts[it.b];
   return x;
@@ -472,7 +475,7 @@ __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& 
   }
 }
 
-template <int NTW>
+template <int NTW, bool MULTI>
 __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const TransferArgs p) {
   __shared__ __attribute__((aligned(16))) unsigned char smem[kSmemBytes];
   uint16_t* Xs = reinterpret_cast<uint16_t*>(smem);
@@ -541,103 +544,124 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   __syncthreads();
   staged = staged && flag[0] == 0;
 
-  // ---- build X[64][d_in] ----
-  if (staged) {
-    const int head = wave / WPH;
-    if (head < H) {
-      const GroupLds L{estart, ecol, ew, einfo, dt, e_base};
-      const int r_first = (wave % WPH) * 8 * RPG + (lane >> 3) * RPG;
-      const int base = gbase[r_first];
-      if (cx.two_tap) {
-        if (unrot) build_groups<true, true, 4>(cx, p, L, base, head, r_first, RPG, lane, Xs);
-        else build_groups<true, false, 4>(cx, p, L, base, head, r_first, RPG, lane, Xs);
-      } else {
-        if (unrot) build_groups<false, true, 4>(cx, p, L, base, head, r_first, RPG, lane, Xs);
-        else build_groups<false, false, 4>(cx, p, L, base, head, r_first, RPG, lane, Xs);
-      }
-    }
-  } else {
-    const int r = tid >> 3;         // 8 threads per row
-    const int e0 = (tid & 7) * 8;   // features e0..e0+7 and e0+64..e0+71 of every head
-    for (int h = 0; h < H; ++h) {
-      float x[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u) x[u] = 0.0f;
-      if (r < nrows) build_row_global(p, cx, g0 + r, h, e0, x);
-      uint16_t* xr = Xs + r * kXF + h * kDH;
-      *reinterpret_cast<uint4*>(xr + e0) = pack8(x);
-      *reinterpret_cast<uint4*>(xr + 64 + e0) = pack8(x + 8);
-    }
-  }
-  __syncthreads();
-
-  // ---- multiply ----
+  f32x16 acc[2][NTW];  // zeroed after the first tap's build
+  // This wave's accumulators: receiver head `head`, n-tiles feat[q].
   const int head = NTW == 4 ? wave : (wave >> 1);
   const int nt0 = NTW == 4 ? 0 : (wave & 1);
   constexpr int NTS = 4 / NTW;  // n-tile stride inside the head
   int feat[NTW];
 #pragma unroll
   for (int q = 0; q < NTW; ++q) feat[q] = 32 * (nt0 + q * NTS);
-  const int KS = H * (kDH / 16);
+  const int KS = H * (kDH / 16);  // k-steps of one tap
   const int NB = p.H_r * (kDH / 32);
   const int lc_store = it.l * 2 + it.c;
-  const bf16x8* W = static_cast<const bf16x8*>(p.Wp) + (long long)lc_store * KS * NB * 64 +
-                    (4 * head + nt0) * 64 + lane;
   const int ks0 = (int)(blockIdx.x % (unsigned)H) * (kDH / 16);  // this workgroup's first k-step
 
-  f32x16 acc[2][NTW];
+  // One pass per tap of the layer map (MULTI: concatenated taps, each one
+  // sender layer): build that tap's X, multiply it by the matching k block of
+  // the map into the same accumulators.  From the second tap on the
+  // accumulators are live during the build, which then keeps fewer loads in
+  // flight.
+  const int n_pass = MULTI ? p.n_taps : 1;
+  for (int tap = 0; tap < n_pass; ++tap) {
+    if (tap > 0) __syncthreads();  // every wave is done reading the previous tap's X
+    const Ctx ct = make_ctx(p, it, tap);
+    // ---- build X[64][d_in] of this tap ----
+    if (staged) {
+      const int sh = wave / WPH;  // sender head this wave builds
+      if (sh < H) {
+        const GroupLds L{estart, ecol, ew, einfo, dt, e_base};
+        const int r_first = (wave % WPH) * 8 * RPG + (lane >> 3) * RPG;
+        const int base = gbase[r_first];
+        if (MULTI) {  // one sender layer per tap
+          if (tap == 0) {
+            if (unrot) build_groups<false, true, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+            else build_groups<false, false, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+          } else {
+            if (unrot) build_groups<false, true, 2>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+            else build_groups<false, false, 2>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+          }
+        } else if (ct.two_tap) {
+          if (unrot) build_groups<true, true, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+          else build_groups<true, false, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+        } else {
+          if (unrot) build_groups<false, true, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+          else build_groups<false, false, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+        }
+      }
+    } else {
+      const int r = tid >> 3;         // 8 threads per row
+      const int e0 = (tid & 7) * 8;   // features e0..e0+7 and e0+64..e0+71 of every head
+      for (int h = 0; h < H; ++h) {
+        float x[16];
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+        for (int u = 0; u < 16; ++u) x[u] = 0.0f;
+        if (r < nrows) build_row_global(p, ct, g0 + r, h, e0, x);
+        uint16_t* xr = Xs + r * kXF + h * kDH;
+        *reinterpret_cast<uint4*>(xr + e0) = pack8(x);
+        *reinterpret_cast<uint4*>(xr + 64 + e0) = pack8(x + 8);
+      }
+    }
+    __syncthreads();
+    if (tap == 0) {
 #pragma unroll
-    for (int q = 0; q < NTW; ++q)
+      for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) acc[mt][q][i] = 0.0f;
+        for (int q = 0; q < NTW; ++q)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[mt][q][i] = 0.0f;
+    }
 
-  bf16x8 wr[4][NTW];  // map fragments of four consecutive k-steps
-  auto kstep = [&](int ks) { int k = ks + ks0; return k >= KS ? k - KS : k; };
-  auto load_w = [&](bf16x8* dst, int ks) {
-    const bf16x8* Wk = W + (long long)kstep(ks) * NB * 64;
+    // ---- multiply ----
+    const bf16x8* W = static_cast<const bf16x8*>(p.Wp) +
+                      ((long long)lc_store * p.n_taps + tap) * KS * NB * 64 + (4 * head + nt0) * 64 +
+                      lane;
+    bf16x8 wr[4][NTW];  // map fragments of four consecutive k-steps
+    auto kstep = [&](int ks) { int k = ks + ks0; return k >= KS ? k - KS : k; };
+    auto load_w = [&](bf16x8* dst, int ks) {
+      const bf16x8* Wk = W + (long long)kstep(ks) * NB * 64;
 #pragma unroll
-    for (int q = 0; q < NTW; ++q) dst[q] = Wk[q * NTS * 64];
-  };
-  auto read_x = [&](bf16x8* xa, int ks) {
-    const int k = kstep(ks);
+      for (int q = 0; q < NTW; ++q) dst[q] = Wk[q * NTS * 64];
+    };
+    auto read_x = [&](bf16x8* xa, int ks) {
+      const int k = kstep(ks);
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-      xa[mt] = *reinterpret_cast<const bf16x8*>(Xs + (32 * mt + (lane & 31)) * kXF + 16 * k +
+      for (int mt = 0; mt < 2; ++mt)
+        xa[mt] = *reinterpret_cast<const bf16x8*>(Xs + (32 * mt + (lane & 31)) * kXF + 16 * k +
                                                 8 * (lane >> 5));
-  };
-  bf16x8 xc[2], xn[2];  // X fragments of this k-step and the next
-  // One k-step: read next X from LDS, multiply, then refill this map slot with
-  // k-step ks + 4.  LOAD is a constant so that the loop body has no branches
-  // and every wait on a map fragment keeps the three younger k-steps in flight.
-  auto step = [&](bf16x8* wf, int ks, auto load) {
-    read_x(xn, ks + 1);
+    };
+    bf16x8 xc[2], xn[2];  // X fragments of this k-step and the next
+    // One k-step: read next X from LDS, multiply, then refill this map slot with
+    // k-step ks + 4.  LOAD is a constant so that the loop body has no branches
+    // and every wait on a map fragment keeps the three younger k-steps in flight.
+    auto step = [&](bf16x8* wf, int ks, auto load) {
+      read_x(xn, ks + 1);
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
+      for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int q = 0; q < NTW; ++q)
-        acc[mt][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[q], xc[mt], acc[mt][q], 0, 0, 0);
-    if (decltype(load)::value) load_w(wf, ks + 4);
-    xc[0] = xn[0];
-    xc[1] = xn[1];
-    __builtin_amdgcn_sched_barrier(0);  // keep the refill in this k-step
-  };
-  using Load = std::true_type;
-  using NoLoad = std::false_type;
+        for (int q = 0; q < NTW; ++q)
+          acc[mt][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[q], xc[mt], acc[mt][q], 0, 0, 0);
+      if (decltype(load)::value) load_w(wf, ks + 4);
+      xc[0] = xn[0];
+      xc[1] = xn[1];
+      __builtin_amdgcn_sched_barrier(0);  // keep the refill in this k-step
+    };
+    using Load = std::true_type;
+    using NoLoad = std::false_type;
 #pragma unroll
-  for (int u = 0; u < 4; ++u) load_w(wr[u], u);  // KS is a multiple of 8
-  read_x(xc, 0);
-  for (int ks = 0; ks < KS - 4; ks += 4) {
-    step(wr[0], ks, Load());
-    step(wr[1], ks + 1, Load());
-    step(wr[2], ks + 2, Load());
-    step(wr[3], ks + 3, Load());
+    for (int u = 0; u < 4; ++u) load_w(wr[u], u);  // KS is a multiple of 8
+    read_x(xc, 0);
+    for (int ks = 0; ks < KS - 4; ks += 4) {
+      step(wr[0], ks, Load());
+      step(wr[1], ks + 1, Load());
+      step(wr[2], ks + 2, Load());
+      step(wr[3], ks + 3, Load());
+    }
+    step(wr[0], KS - 4, NoLoad());
+    step(wr[1], KS - 3, NoLoad());
+    step(wr[2], KS - 2, NoLoad());
+    step(wr[3], KS - 1, NoLoad());
   }
-  step(wr[0], KS - 4, NoLoad());
-  step(wr[1], KS - 3, NoLoad());
-  step(wr[2], KS - 2, NoLoad());
-  step(wr[3], KS - 1, NoLoad());
   __syncthreads();  // every wave is done reading X; the X region is free
 
   // ---- store ----
@@ -736,13 +760,12 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_direct_kernel(const Tran
   __shared__ __attribute__((aligned(16))) uint16_t lds[LDS];
 
   const Item it = decode_item(p, blockIdx.x);
-  const Ctx cx = make_ctx(p, it);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int j0 = it.tile * MT;
   const int Tr = p.Tr[it.b];
   const int row0 = p.row0[it.b];
-  const int KS = p.H_s * (kDH / 16);
+  const int KS = p.n_taps * p.H_s * (kDH / 16);  // k-steps of the whole map row
   const int NB = p.H_r * (kDH / 32);
   const int lc_store = it.l * 2 + it.c;
   const bf16x8* W = static_cast<const bf16x8*>(p.Wp) + (long long)lc_store * KS * NB * 64 +
@@ -758,8 +781,11 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_direct_kernel(const Tran
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[mt][nt][i] = 0.0f;
 
-  for (int h = 0; h < p.H_s; ++h) {
-    uint16_t* xb = lds + (h & 1) * XBUF;
+  // v runs over (tap, sender head) pairs: the k blocks of the map row
+  for (int v = 0; v < p.n_taps * p.H_s; ++v) {
+    const int h = v % p.H_s;
+    const Ctx cx = make_ctx(p, it, v / p.H_s);
+    uint16_t* xb = lds + (v & 1) * XBUF;
 #pragma unroll
     for (int q = 0; q < WM; ++q) {
       const int r = brow + 64 * q;
@@ -771,7 +797,7 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_direct_kernel(const Tran
       *reinterpret_cast<uint4*>(xb + r * kXS + e0 + 64) = pack8(x + 8);
     }
     __syncthreads();
-    const bf16x8* Wh = W + (long long)h * 8 * NB * 64;
+    const bf16x8* Wh = W + (long long)v * 8 * NB * 64;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       bf16x8 xa[2], wf[4];
@@ -814,7 +840,8 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
   const Item it = decode_item(p, blockIdx.x);
   const int RT = p.rows_per_tile;
   const int d = p.d_h, half = d / 2;
-  const int d_in = p.H_s * d, d_r = p.H_r * d;
+  const int NV = p.n_taps * p.H_s;  // (tap, sender head) blocks of the map row
+  const int d_in = NV * d, d_r = p.H_r * d;
   const int j0 = it.tile * RT;
   const int Tr = p.Tr[it.b], Ts = p.Ts[it.b];
   const bool keys = it.c == 0;
@@ -822,14 +849,16 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
   const float wlo = p.wlo[it.l], whi = p.whi[it.l];
   const bool two_tap = whi != 0.0f;
   const float* Sb = static_cast<const float*>(p.S) + it.b * p.s_sb + it.c * p.s_sc;
-  const float* S_lo = Sb + (long long)p.lo[it.l] * p.s_sl;
-  const float* S_hi = Sb + (long long)p.hi[it.l] * p.s_sl;
   const int lc_store = it.l * 2 + it.c;
 
-  for (int idx = threadIdx.x; idx < RT * p.H_s * half; idx += kF32Threads) {
-    const int r = idx / (p.H_s * half);
-    const int rem = idx - r * (p.H_s * half);
-    const int h = rem / half, f = rem - h * half;
+  for (int idx = threadIdx.x; idx < RT * NV * half; idx += kF32Threads) {
+    const int r = idx / (NV * half);
+    const int rem = idx - r * (NV * half);
+    const int vh = rem / half, f = rem - vh * half;
+    const int h = vh % p.H_s, t = vh / p.H_s;
+    const int lo = p.concat ? p.taps[it.l][t] : p.lo[it.l];
+    const float* S_lo = Sb + (long long)lo * p.s_sl;
+    const float* S_hi = Sb + (long long)(p.concat ? lo : p.hi[it.l]) * p.s_sl;
     const int j = j0 + r;
     float x1 = 0.f, x2 = 0.f;
     if (j < Tr) {
@@ -856,8 +885,8 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
         x2 = fmaf(w, m2, x2);
       }
     }
-    xs[r * d_in + h * d + f] = x1;
-    xs[r * d_in + h * d + f + half] = x2;
+    xs[r * d_in + vh * d + f] = x1;
+    xs[r * d_in + vh * d + f + half] = x2;
   }
   __syncthreads();
 
@@ -907,9 +936,10 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
 
 }  // namespace
 
-int transfer_rows_per_tile(int dtype, int H_r, int d_in) {
+int transfer_rows_per_tile(int dtype, int H_r, int H_s, int n_taps, int d_h) {
   if (dtype == HF_BF16)
-    return ((H_r == 4 || H_r == 8) && d_in <= kHMax * kDH) ? 64 : 64 * (8 / (H_r > 0 ? H_r : 1));
+    return ((H_r == 4 || H_r == 8) && H_s <= kHMax) ? 64 : 64 * (8 / (H_r > 0 ? H_r : 1));
+  const int d_in = n_taps * H_s * d_h;
   int rt = 8192 / (d_in > 0 ? d_in : 1);  // fp32 X tile <= 32 KB of LDS
   return rt < 1 ? 1 : (rt > 16 ? 16 : rt);
 }
@@ -947,17 +977,23 @@ hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s) {
     switch (a.H_r) {
       case 2: hipLaunchKernelGGL(transfer_bf16_direct_kernel<2>, grid, dim3(512), 0, s, a); break;
       case 4:
-        if (a.H_s <= kHMax) hipLaunchKernelGGL(transfer_bf16_tiled_kernel<2>, grid, dim3(512), 0, s, a);
+        if (a.H_s <= kHMax && a.concat)
+          hipLaunchKernelGGL((transfer_bf16_tiled_kernel<2, true>), grid, dim3(512), 0, s, a);
+        else if (a.H_s <= kHMax)
+          hipLaunchKernelGGL((transfer_bf16_tiled_kernel<2, false>), grid, dim3(512), 0, s, a);
         else hipLaunchKernelGGL(transfer_bf16_direct_kernel<4>, grid, dim3(512), 0, s, a);
         break;
       case 8:
-        if (a.H_s <= kHMax) hipLaunchKernelGGL(transfer_bf16_tiled_kernel<4>, grid, dim3(512), 0, s, a);
+        if (a.H_s <= kHMax && a.concat)
+          hipLaunchKernelGGL((transfer_bf16_tiled_kernel<4, true>), grid, dim3(512), 0, s, a);
+        else if (a.H_s <= kHMax)
+          hipLaunchKernelGGL((transfer_bf16_tiled_kernel<4, false>), grid, dim3(512), 0, s, a);
         else hipLaunchKernelGGL(transfer_bf16_direct_kernel<8>, grid, dim3(512), 0, s, a);
         break;
       default: return hipErrorInvalidValue;
     }
   } else {
-    const size_t shmem = (size_t)a.rows_per_tile * a.H_s * a.d_h * sizeof(float);
+    const size_t shmem = (size_t)a.rows_per_tile * a.n_taps * a.H_s * a.d_h * sizeof(float);
     hipLaunchKernelGGL(transfer_f32_kernel, grid, dim3(kF32Threads), shmem, s, a);
   }
   return hipGetLastError();

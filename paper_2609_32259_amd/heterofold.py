@@ -66,6 +66,7 @@ _SIGNATURES = {
     "hf_validate_offsets_host": (C.c_int32, [C.c_int32, _I32P, _I32P]),
     "hf_build_layer_map": (C.c_int32, [C.c_int32, C.c_int32, C.c_int32, _I32P, _I32P, _I32P,
                                        _I32P]),
+    "hf_build_layer_taps": (C.c_int32, [C.c_int32, C.c_int32, _I32P]),
     "hf_packed_maps_bytes": (C.c_size_t, [C.c_int32, C.c_int32, C.c_int32, C.c_int32]),
     "hf_pack_maps": (C.c_int32, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
                                  C.c_void_p, C.c_void_p]),
@@ -76,9 +77,16 @@ _SIGNATURES = {
                                    C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc), C.c_void_p,
                                    C.c_void_p, C.POINTER(hf_rope), C.c_void_p, C.c_size_t,
                                    C.c_void_p]),
+    "hf_transfer_kv_taps": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p,
+                                        C.c_void_p, C.c_void_p, C.c_int32, _I32P,
+                                        C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc), C.c_void_p,
+                                        C.c_void_p, C.POINTER(hf_rope), C.c_void_p, C.c_size_t,
+                                        C.c_void_p]),
     "hf_profiler_enable": (C.c_int32, [C.c_int32]),
     "hf_profiler_reset": (C.c_int32, []),
     "hf_profiler_query": (C.c_int32, [C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
+    "hf_profiler_samples": (C.c_int32, [C.c_int32, C.POINTER(C.c_float), C.c_int64,
+                                        C.POINTER(C.c_int64)]),
 }
 
 _lib = None
@@ -221,6 +229,13 @@ def hf_build_layer_map(L_s: int, L_r: int, mode: int = HF_LAYERS_INTERP2):
     return tuple(o[:L_r] for o in out)
 
 
+def hf_build_layer_taps(L_s: int, L_r: int):
+    """The paper's three-layer neighbourhood: host int32 numpy [L_r, 3]."""
+    out = np.zeros((max(L_r, 1), 3), dtype=np.int32)
+    _check(lib().hf_build_layer_taps(int(L_s), int(L_r), _p32(out)), "hf_build_layer_taps")
+    return out[:L_r]
+
+
 # ---------------------------------------------------------------------------
 # Maps and transfer
 # ---------------------------------------------------------------------------
@@ -323,6 +338,37 @@ def hf_transfer_kv(s_len, r_len, alignment: Alignment, layer_map, S, R, A_packed
     return R
 
 
+def hf_transfer_kv_taps(s_len, r_len, alignment: Alignment, taps, S, R, A_packed, bias=None,
+                        rope=None, workspace=None, stream=None):
+    """hf_transfer_kv with concatenated-tap maps: taps is the host table
+    [L_r, n_taps] (e.g. hf_build_layer_taps) and A_packed packs maps of input
+    size n_taps * H_s * d_h."""
+    torch = _torch()
+    s_len, r_len = _i32(s_len), _i32(r_len)
+    taps = np.ascontiguousarray(np.asarray(taps, dtype=np.int32))
+    if taps.ndim != 2:
+        raise TypeError("taps must be a table [L_r, n_taps]")
+    sd, rd = kv_desc(S), kv_desc(R)
+    rs, keep = _rope_struct(rope)
+    wsb = hf_transfer_workspace_bytes(s_len, r_len, S, R, rope)
+    if workspace is None and wsb > 0:
+        workspace = torch.empty(wsb, dtype=torch.uint8, device=S.device)
+    if bias is not None and (bias.dtype != torch.float32 or not bias.is_contiguous()):
+        raise TypeError("bias must be a contiguous fp32 tensor [L_r, 2, d_r]")
+    st = lib().hf_transfer_kv_taps(
+        s_len.size, _p32(s_len), _p32(r_len), _dev_i32(alignment.row_ptr, "row_ptr"),
+        _dev_i32(alignment.col, "col"), _dev_i32(alignment.num, "num"),
+        _dev_i32(alignment.den, "den"), int(taps.shape[1]), _p32(taps),
+        C.byref(sd), C.byref(rd), C.c_void_p(A_packed.data_ptr()),
+        C.c_void_p(bias.data_ptr()) if bias is not None else None,
+        C.byref(rs) if rs is not None else None,
+        C.c_void_p(workspace.data_ptr()) if workspace is not None else None,
+        int(workspace.numel() * workspace.element_size()) if workspace is not None else 0,
+        _stream(stream))
+    _check(st, "hf_transfer_kv_taps")
+    return R
+
+
 # ---------------------------------------------------------------------------
 # Profiler
 # ---------------------------------------------------------------------------
@@ -339,3 +385,13 @@ def hf_profiler_query(kernel_id: int):
     ms, n = C.c_double(0.0), C.c_int64(0)
     _check(lib().hf_profiler_query(int(kernel_id), C.byref(ms), C.byref(n)), "hf_profiler_query")
     return float(ms.value), int(n.value)
+
+
+def hf_profiler_samples(kernel_id: int) -> np.ndarray:
+    """Per-launch durations (ms) of one kernel since the last reset."""
+    n = C.c_int64(0)
+    _check(lib().hf_profiler_samples(int(kernel_id), None, 0, C.byref(n)), "hf_profiler_samples")
+    out = np.zeros(max(n.value, 1), dtype=np.float32)
+    _check(lib().hf_profiler_samples(int(kernel_id), out.ctypes.data_as(C.POINTER(C.c_float)),
+                                     out.size, C.byref(n)), "hf_profiler_samples")
+    return out[:n.value]

@@ -4,7 +4,8 @@
 path need -- the character spans on the device, the alignment table, the
 packed maps, the receiver cache and the workspaces -- and ``step()`` runs the
 path once: ``hf_build_alignment`` -> ``hf_build_layer_map`` ->
-``hf_transfer_kv``.  It does no arithmetic of the method itself.
+``hf_transfer_kv`` (with ``layer_map="neighbor3"``: ``hf_build_layer_taps`` ->
+``hf_transfer_kv_taps``).  It does no arithmetic of the method itself.
 """
 
 from __future__ import annotations
@@ -18,10 +19,13 @@ from . import heterofold as hf
 
 class TransferPath:
     def __init__(self, seg, S, A, bias, rope: Optional[dict], L_r: int, H_r: int,
-                 mode: str = "overlap", R=None, pack_stream=None):
+                 mode: str = "overlap", R=None, pack_stream=None, layer_map: str = "interp2"):
         import torch
 
+        if layer_map not in ("interp2", "neighbor3"):
+            raise ValueError(f"layer map {layer_map!r} unknown")
         self.torch = torch
+        self.layer_mode = layer_map
         dev = S.device
         self.seg = seg
         self.mode = mode
@@ -67,10 +71,17 @@ class TransferPath:
                                      workspace=self.align_ws, stream=stream)
 
     def build_layer_map(self):
-        self.layer_map = hf.hf_build_layer_map(self.L_s, self.L_r)
+        if self.layer_mode == "neighbor3":
+            self.layer_map = hf.hf_build_layer_taps(self.L_s, self.L_r)
+        else:
+            self.layer_map = hf.hf_build_layer_map(self.L_s, self.L_r)
         return self.layer_map
 
     def transfer(self, stream=None):
+        if self.layer_mode == "neighbor3":
+            return hf.hf_transfer_kv_taps(self.s_len, self.r_len, self.alignment, self.layer_map,
+                                          self.S, self.R, self.A_packed, self.bias, self.rope,
+                                          workspace=self.transfer_ws, stream=stream)
         return hf.hf_transfer_kv(self.s_len, self.r_len, self.alignment, self.layer_map, self.S,
                                  self.R, self.A_packed, self.bias, self.rope,
                                  workspace=self.transfer_ws, stream=stream)

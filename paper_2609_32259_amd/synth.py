@@ -50,10 +50,20 @@ class Config:
     bias_var: float = 0.05
     rope: Optional[Tuple[float, float]] = None   # (theta_s, theta_r): keys stored post-RoPE
     batch: int = 1
+    layer_map: str = "interp2"      # "interp2" or "neighbor3" (three concatenated sender layers)
 
     @property
     def d_in(self) -> int:
         return self.H_s * self.d_h
+
+    @property
+    def n_taps(self) -> int:
+        return 3 if self.layer_map == "neighbor3" else 1
+
+    @property
+    def d_map_in(self) -> int:
+        """Input size of each map: the concatenated features of n_taps layers."""
+        return self.n_taps * self.d_in
 
     @property
     def d_r(self) -> int:
@@ -75,6 +85,9 @@ LLAMA8B_QWEN7B_4K = Config("llama8b->qwen7b-shape T_s=4096", "bf16", L_s=32, L_r
 LLAMA8B_14B_8K = Config("llama8b->14b-shape T_s=8192 rope", "bf16", L_s=32, L_r=40, H_s=8,
                         H_r=8, d_h=128, T_s=8192, bias_var=0.05, rope=(5.0e5, 1.0e9))
 LLAMA8B_14B_32K = LLAMA8B_14B_8K.with_(name="llama8b->14b-shape T_s=32768 rope", T_s=32768)
+# The same shape with the paper's three-layer neighbourhood map (A is d_r x 3 d_in).
+LLAMA8B_14B_32K_N3 = LLAMA8B_14B_32K.with_(name="llama8b->14b-shape T_s=32768 rope neighbor3",
+                                           layer_map="neighbor3")
 # Qwen-7B -> Llama-8B shape (layer upsampling), batch of 4, theta 1e6 -> 5e5.
 QWEN7B_LLAMA8B_B4 = Config("qwen7b->llama8b-shape B=4 rope", "bf16", L_s=28, L_r=32, H_s=4,
                            H_r=8, d_h=128, T_s=4096, bias_var=0.05, rope=(1.0e6, 5.0e5),
@@ -85,6 +98,7 @@ CONFIGS = {
     "qwen7b-4k": LLAMA8B_QWEN7B_4K,
     "14b-8k": LLAMA8B_14B_8K,
     "14b-32k": LLAMA8B_14B_32K,
+    "14b-32k-n3": LLAMA8B_14B_32K_N3,
     "reverse-b4": QWEN7B_LLAMA8B_B4,
 }
 
@@ -267,13 +281,14 @@ def make_cache(cfg: Config, seg: Segmentation, seed: int = 0, device="cpu"):
 
 
 def make_maps(cfg: Config, seed: int = 0, device="cpu"):
-    """A [L_r, 2, d_r, d_in] ~ N(0, 1/d_in) in the storage dtype and bias
-    [L_r, 2, d_r] ~ N(0, bias_var) in fp32."""
+    """A [L_r, 2, d_r, n] ~ N(0, 1/n) with n = cfg.d_map_in, in the storage
+    dtype, and bias [L_r, 2, d_r] ~ N(0, bias_var) in fp32."""
     torch = _torch()
     _, _, _, map_seq = _child_seeds(seed, 4)
     g = _torch_gen(map_seq, device)
-    A = torch.randn((cfg.L_r, 2, cfg.d_r, cfg.d_in), generator=g, dtype=torch.float32,
-                    device=device) * (1.0 / np.sqrt(cfg.d_in))
+    n = cfg.d_map_in
+    A = torch.randn((cfg.L_r, 2, cfg.d_r, n), generator=g, dtype=torch.float32,
+                    device=device) * (1.0 / np.sqrt(n))
     bias = torch.randn((cfg.L_r, 2, cfg.d_r), generator=g, dtype=torch.float32,
                        device=device) * float(np.sqrt(cfg.bias_var))
     return A.to(storage_dtype(cfg)), bias

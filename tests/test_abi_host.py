@@ -165,3 +165,46 @@ def test_profiler_host_calls(L):
     assert hf.hf_profiler_query(hf.HF_KERNEL_TRANSFER) == (0.0, 0)
     with pytest.raises(hf.HeteroFoldError):
         hf.hf_profiler_query(99)
+    assert hf.hf_profiler_samples(hf.HF_KERNEL_TRANSFER).size == 0
+    with pytest.raises(hf.HeteroFoldError):
+        hf.hf_profiler_samples(-1)
+
+
+@pytest.mark.parametrize("L_s,L_r", [(32, 40), (32, 28), (28, 32), (36, 32), (40, 36), (4, 6),
+                                     (9, 9), (1, 3), (5, 1), (3, 20), (64, 7)])
+def test_layer_taps_match_oracle(L, L_s, L_r):
+    """hf_build_layer_taps against the oracle's Eq. 1 table (itself pinned by
+    the worked rows and the App. B.4 parameter counts)."""
+    assert np.array_equal(hf.hf_build_layer_taps(L_s, L_r), lm.neighbor3(L_s, L_r))
+
+
+def test_layer_taps_errors(L):
+    with pytest.raises(hf.HeteroFoldError) as ei:
+        hf.hf_build_layer_taps(0, 3)
+    assert ei.value.status == -2
+    assert L.hf_build_layer_taps(3, 3, None) == -1
+
+
+def test_transfer_taps_host_validation(L):
+    s_len = np.array([64], np.int32)
+    r_len = np.array([60], np.int32)
+    taps = np.ascontiguousarray(lm.neighbor3(4, 6), dtype=np.int32)
+    fake = C.c_void_p(0x1000)
+
+    def call(n=3, tp=taps, sd=None, rd=None):
+        sd = sd or _desc()
+        rd = rd or _desc(L_=6)
+        return L.hf_transfer_kv_taps(1, _p(s_len), _p(r_len), fake, fake, fake, fake, n,
+                                     _p(tp) if tp is not None else None, C.byref(sd),
+                                     C.byref(rd), fake, None, None, None, 0, None)
+
+    assert call(tp=None) == -1
+    assert call(n=0) == -2
+    assert call(n=4) == -2
+    bad = taps.copy()
+    bad[5, 2] = 4
+    assert call(tp=bad) == -2                                  # sender layer out of range
+    bad = taps.copy()
+    bad[1, 0] = -1
+    assert call(tp=bad) == -2
+    assert call(sd=_desc(d=64), rd=_desc(L_=6, d=64)) == -8    # bf16 needs d_h = 128

@@ -1,0 +1,195 @@
+"""GPU parity of the concatenated-tap transfer (the paper's three-layer
+neighbourhood map, Sec. 3.1 Eq. 1-2): hf_transfer_kv_taps against the fp64
+oracle ``transfer_taps``.  Small cases element by element over every layer,
+role and row; the full-size 32K workload on sampled rows in the launch
+configuration the benchmark times."""
+
+import numpy as np
+import pytest
+
+from oracle import alignment as al
+from oracle import layer_map as lm
+from oracle import transfer as tr
+from paper_2609_32259_amd import synth
+
+from _parity import check_layer
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch
+    assert torch.cuda.is_available(), "GPU test needs a GPU"
+    from paper_2609_32259_amd import heterofold
+    heterofold.lib()
+    return torch
+
+
+def _np64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _run(torch, cfg, wl, mode, taps, R=None):
+    from paper_2609_32259_amd import heterofold as hf
+    from paper_2609_32259_amd.path import TransferPath
+    path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r, mode=mode, R=R,
+                        layer_map="neighbor3")
+    path.build_alignment()
+    if taps is None:
+        path.build_layer_map()
+    else:
+        path.layer_map = np.asarray(taps, np.int32)
+    path.transfer()
+    torch.cuda.synchronize()
+    return path
+
+
+def _compare_full(torch, cfg, wl, mode="overlap", taps=None, qlimited_k=False):
+    taps_np = lm.neighbor3(cfg.L_s, cfg.L_r) if taps is None else np.asarray(taps)
+    print(f"[gpu-taps] {cfg.name} mode={mode} B={wl.seg.batch} T_r={list(wl.seg.r_len)} "
+          f"n_taps={taps_np.shape[1]} rope={wl.rope is not None}", flush=True)
+    path = _run(torch, cfg, wl, mode, taps)
+    worst = (0.0, 0.0)
+    for b in range(wl.seg.batch):
+        T_r = int(wl.seg.r_len[b])
+        if T_r == 0:
+            continue
+        sb, se, rb, re_ = wl.seg.seq(b)
+        csr = al.build_alignment(sb, se, rb, re_, mode)
+        T_s = int(wl.seg.s_len[b])
+        S = _np64(wl.S[b, :, :, :, :T_s, :])
+        rp = None
+        if wl.rope is not None:
+            rp = dict(wl.rope)
+            for k in ("pos0_s", "pos0_r"):
+                rp[k] = 0 if wl.rope.get(k) is None else int(np.asarray(wl.rope[k])[b])
+        bias = None if wl.bias is None else _np64(wl.bias)
+        ref = tr.transfer_taps(S, taps_np, csr, _np64(wl.A), bias, rp, H_r=cfg.H_r)
+        got = _np64(path.R[b, :, :, :, :T_r, :])
+        for l in range(cfg.L_r):
+            for c in range(2):
+                ql = qlimited_k and c == 0
+                x = tr.features_taps(S, taps_np, csr, None, l, c) if ql else None
+                rel, mx = check_layer(got[l, c], ref[l, c], f"{cfg.name} b={b} l={l} c={c}",
+                                      dtype=cfg.dtype, quantization_limited=ql, x=x,
+                                      A=_np64(wl.A[l, c]) if ql else None)
+                worst = (max(worst[0], rel), max(worst[1], mx))
+    print(f"[gpu-taps]   worst rel-Fro {worst[0]:.3e}, max|err| {worst[1]:.3e}", flush=True)
+
+
+@pytest.mark.parametrize("mode", ["overlap", "ta"])
+def test_taps_fp32(torch, mode):
+    cfg = synth.TINY_F32.with_(name="tiny-f32 neighbor3", layer_map="neighbor3", L_s=11)
+    wl = synth.make_workload(cfg, seed=20, device="cuda")
+    _compare_full(torch, cfg, wl, mode)
+
+
+def test_taps_bf16_14b_shape_small(torch):
+    cfg = synth.LLAMA8B_14B_8K.with_(name="14b n3 small", layer_map="neighbor3", T_s=300, L_r=6)
+    wl = synth.make_workload(cfg, seed=21, device="cuda")
+    _compare_full(torch, cfg, wl, "overlap")
+    _compare_full(torch, cfg, wl, "ta")
+
+
+def test_taps_bf16_four_receiver_heads_outlier_keys(torch):
+    cfg = synth.LLAMA8B_QWEN7B_4K.with_(name="qwen7b n3 small", layer_map="neighbor3", T_s=400,
+                                        L_r=5)
+    wl = synth.make_workload(cfg, seed=22, device="cuda")
+    _compare_full(torch, cfg, wl, "overlap", qlimited_k=True)
+
+
+def test_taps_bf16_two_receiver_heads(torch):
+    cfg = synth.LLAMA8B_14B_8K.with_(name="8->2 heads n3", layer_map="neighbor3", H_r=2, L_r=3,
+                                     T_s=500)
+    wl = synth.make_workload(cfg, seed=23, device="cuda")
+    _compare_full(torch, cfg, wl, "overlap")
+
+
+def test_taps_bf16_reverse_batched(torch):
+    cfg = synth.QWEN7B_LLAMA8B_B4.with_(name="reverse n3", layer_map="neighbor3", L_r=5)
+    parts = []
+    rng = np.random.default_rng(24)
+    for T in (70, 1, 260):
+        sb, se = synth.segment_tokens(rng, T, *cfg.s_len)
+        rb, re_ = synth.segment_chars(rng, int(se[-1]), *cfg.r_len)
+        parts.append((sb, se, rb, re_))
+    seg = synth.concat_segmentations(parts)
+    S = synth.make_cache(cfg, seg, seed=24, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=24, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=np.array([4, 0, 90], np.int32),
+                             pos0_r=np.array([0, 2, 17], np.int32))
+    _compare_full(torch, cfg, synth.Workload(cfg, seg, S, A, bias, rope), "overlap")
+
+
+@pytest.mark.parametrize("n_taps", [1, 2])
+def test_taps_bf16_other_tap_counts(torch, n_taps):
+    base = synth.LLAMA8B_14B_8K.with_(name=f"14b {n_taps} taps", T_s=200, L_r=4)
+    cfg = base.with_(layer_map="neighbor3")
+    seg = synth.make_segmentation(cfg, seed=25)
+    S = synth.make_cache(cfg, seg, seed=25, device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(25)
+    A = (torch.randn((cfg.L_r, 2, cfg.d_r, n_taps * cfg.d_in), generator=g, device="cuda")
+         / np.sqrt(n_taps * cfg.d_in)).to(torch.bfloat16)
+    _, bias = synth.make_maps(cfg, seed=25, device="cuda")
+    taps = np.array([[0, 31, 7][:n_taps], [5, 5, 5][:n_taps], [31, 0, 16][:n_taps],
+                     [12, 13, 14][:n_taps]], np.int32)
+    _compare_full(torch, cfg, synth.Workload(cfg, seg, S, A, bias, synth.rope_params(cfg)),
+                  "overlap", taps=taps)
+
+
+def test_taps_bf16_beyond_staging_capacity(torch):
+    cfg = synth.LLAMA8B_14B_8K.with_(name="n3 unstaged", layer_map="neighbor3", L_r=3)
+    rng = np.random.default_rng(26)
+    sb1, se1 = synth.segment_tokens(rng, 150, 1, 7)
+    sb2, se2 = synth.segment_tokens(rng, 800, 1, 2)
+    sb = np.concatenate([sb1, sb2 + se1[-1]]).astype(np.int32)
+    se = np.concatenate([se1, se2 + se1[-1]]).astype(np.int32)
+    rb1, re1 = synth.segment_chars(rng, int(se1[-1]), 1, 8)
+    rl = rng.integers(8, 17, 400)
+    re2 = (np.cumsum(rl) + se1[-1]).astype(np.int32)
+    re2 = re2[re2 <= se[-1]]
+    rb2 = np.concatenate([[se1[-1]], re2[:-1]]).astype(np.int32)
+    seg = synth.concat_segmentations([(sb, se, np.concatenate([rb1, rb2]).astype(np.int32),
+                                       np.concatenate([re1, re2]).astype(np.int32))])
+    S = synth.make_cache(cfg, seg, seed=26, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=26, device="cuda")
+    _compare_full(torch, cfg, synth.Workload(cfg, seg, S, A, bias, synth.rope_params(cfg)),
+                  "overlap")
+
+
+def test_taps_bf16_identity_first_block_is_bit_exact(torch):
+    cfg = synth.LLAMA8B_14B_8K.with_(name="n3 identity", layer_map="neighbor3", L_s=9, L_r=9,
+                                     T_s=150, rope=None)
+    wl = synth.make_workload(cfg, seed=27, device="cuda")
+    seg = synth.concat_segmentations([(wl.seg.s_beg, wl.seg.s_end, wl.seg.s_beg, wl.seg.s_end)])
+    A = torch.zeros((cfg.L_r, 2, cfg.d_r, 3 * cfg.d_in), dtype=torch.bfloat16, device="cuda")
+    A[..., :cfg.d_in] = torch.eye(cfg.d_r, dtype=torch.bfloat16, device="cuda")
+    wl = synth.Workload(cfg, seg, wl.S, A, None, None)
+    taps = lm.neighbor3(cfg.L_s, cfg.L_r)
+    for mode in ("overlap", "ta"):
+        R = _run(torch, cfg, wl, mode, None).R
+        for l in range(cfg.L_r):
+            assert torch.equal(R[0, l, :, :, :150, :].view(torch.int16),
+                               wl.S[0, int(taps[l, 0]), :, :, :150, :].view(torch.int16))
+
+
+def test_full_14b_shape_32k_neighbor3(torch):
+    """The benchmark's neighbourhood-map workload, sampled rows."""
+    cfg = synth.LLAMA8B_14B_32K_N3
+    wl = synth.make_workload(cfg, seed=0, device="cuda")
+    print(f"[gpu-taps] full-size {cfg.name} T_r={list(wl.seg.r_len)}", flush=True)
+    path = _run(torch, cfg, wl, "overlap", None)
+    taps = lm.neighbor3(cfg.L_s, cfg.L_r)
+    T_r = int(wl.seg.r_len[0])
+    rng = np.random.default_rng(98)
+    rows = sorted({0, 1, 63, 64, T_r // 2, T_r - 2, T_r - 1, *rng.integers(0, T_r, 20).tolist()})
+    csr = al.build_alignment(*wl.seg.seq(0), "overlap")
+    rp = dict(wl.rope, pos0_s=0, pos0_r=0)
+    get = lambda l, c, idx: _np64(wl.S[0, l, c][:, torch.as_tensor(idx, device="cuda"), :])  # noqa: E731
+    for l in (0, 2, 20, 39):
+        for c in (0, 1):
+            ref = tr.transfer_rows_taps(get, taps, csr, _np64(wl.A[l, c]), _np64(wl.bias[l, c]),
+                                        rp, cfg.d_h, l, c, rows)
+            got = _np64(path.R[0, l, c][:, torch.as_tensor(rows, device="cuda"), :])
+            check_layer(got, ref, f"{cfg.name} l={l} c={c} rows={len(rows)}")
