@@ -12,13 +12,20 @@ For one sequence, receiver layer l, role c in {K=0, V=1} and receiver token j:
 3. Token alignment: x_j = sum over the CSR row of (num / den_j) * u_i,
    flattened head-major (feature index h * d_h + e) -- the flattened role-c
    KV feature of Sec. 3.1 (Eq. 2 with one interpolated tap).
-4. Folded affine map of Eq. 9, written in column form: y_j = A[l, c] x_j
+4. Folded affine map of Eq. 9, written in column form: y_j = A[l, c] (x_j / r)
    + b[l, c] with A stored [d_R, d_S] (the transpose of the paper's row-vector
-   A_final) and the scalar 1/r of Eq. 3 folded into A by the caller.
-5. Reshape into receiver KV heads and, for keys, apply the receiver's RoPE at
-   q_j = pos0_r + j with the receiver's theta (Sec. 3.3 "Folding for
-   inference"; App. B.1).
+   A_final).  The scalar r of Eq. 3 is given per (layer, role) as inv_r =
+   1/r (absent: 1, i.e. folded into A by the caller).
+5. Reshape into receiver KV heads.  For keys, apply the receiver's key
+   normalization when given -- RMSNorm over each head's d_h features with
+   weight g[l] and epsilon eps: y <- y / sqrt(mean(y^2) + eps) * g -- and
+   then the receiver's RoPE at q_j = pos0_r + j with the receiver's theta
+   (Sec. 3.3 "Folding for inference"; App. B.1: keys are mapped before key
+   normalization and RoPE, which the receiver applies once).
 6. R[l, c, h', j, e'] = y_j[h' * d_h + e'].
+
+The optional inv_r / key normalization come in an ``opts`` dict:
+``{"inv_r": [L_R, 2] or None, "k_norm": [L_R, d_h] or None, "k_norm_eps": e}``.
 
 Inputs are the exact stored values widened to fp64; the result stays fp64.
 """
@@ -32,6 +39,17 @@ from . import rope as _rope
 from .layer_map import interp2_weights
 
 K, V = 0, 1
+
+
+def rms_norm(y, g, eps):
+    """RMSNorm over the last axis (one receiver head's d_h features)."""
+    y = np.asarray(y, dtype=np.float64)
+    return y / np.sqrt(np.mean(y * y, axis=-1, keepdims=True) + float(eps)) * np.asarray(g, np.float64)
+
+
+def _opts(opts):
+    opts = opts or {}
+    return opts.get("inv_r"), opts.get("k_norm"), float(opts.get("k_norm_eps", 1e-6))
 
 
 def _mix(S_lo, S_hi, a_lo, a_hi, rem):
@@ -63,7 +81,7 @@ def features(S, layer_table, csr, rope, layer, role):
     return _weights_matrix(csr, T_s) @ u
 
 
-def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None):
+def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None, opts=None):
     """Whole receiver cache of one sequence.
 
     S           fp64-convertible [L_S, 2, H_S, T_S, d_h]
@@ -72,8 +90,10 @@ def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None):
     A           [L_R, 2, d_R, d_S];  b  [L_R, 2, d_R] or None
     rope        None or dict(theta_s, theta_r, unrotate_sender_k,
                 rotate_receiver_k, pos0_s, pos0_r)
+    opts        None or dict(inv_r, k_norm, k_norm_eps) (module docstring)
     returns     [L_R, 2, H_R, T_R, d_h] fp64
     """
+    inv_r, k_norm, eps = _opts(opts)
     S = np.asarray(S, dtype=np.float64)
     A = np.asarray(A, dtype=np.float64)
     L_s, _, H_s, T_s, d_h = S.shape
@@ -86,10 +106,14 @@ def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None):
     for l in range(L_r):
         for c in (K, V):
             x = features(S, layer_table, csr, rope, l, c)                  # [T_r, d_S]
+            if inv_r is not None:
+                x = x * float(np.asarray(inv_r, np.float64)[l, c])
             y = x @ A[l, c].T
             if b is not None:
                 y = y + np.asarray(b, dtype=np.float64)[l, c][None, :]
             y = y.reshape(T_r, H_r, d_h).transpose(1, 0, 2)                 # [H_r,T_r,d_h]
+            if c == K and k_norm is not None:
+                y = rms_norm(y, np.asarray(k_norm)[l], eps)
             if c == K and rope is not None and rope.get("rotate_receiver_k", False):
                 y = _rope.rotate(y, rope.get("pos0_r", 0) + np.arange(T_r), rope["theta_r"])
             out[l, c] = y
@@ -97,15 +121,16 @@ def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None):
 
 
 def transfer_rows(get_sender, layer_table, csr, A_lc, b_lc, rope, d_h,
-                  layer, role, rows, return_features=False):
+                  layer, role, rows, return_features=False, opts=None):
     """Selected receiver rows of one (layer, role), entry by entry.
 
     get_sender(l, c, idx) -> fp64 [H_S, len(idx), d_h] gives sender rows idx
     of sender layer l, role c (only the rows the CSR entries name are asked
     for).  A_lc is A[layer, role] ([d_R, d_S]); b_lc its bias or None.
     Returns fp64 [H_R, len(rows), d_h] (and the features x, fp64
-    [len(rows), d_S], when return_features).
+    [len(rows), d_S], when return_features).  opts as in ``transfer``.
     """
+    inv_r, k_norm, eps = _opts(opts)
     lo, hi, rem, den_l = (np.asarray(t) for t in layer_table)
     a_lo, a_hi = interp2_weights(lo, hi, rem, den_l)
     row_ptr, col, num, den = (np.asarray(t, dtype=np.int64) for t in csr)
@@ -131,11 +156,15 @@ def transfer_rows(get_sender, layer_table, csr, A_lc, b_lc, rope, d_h,
                 p = rope.get("pos0_s", 0) + int(col[e])
                 m = _rope.unrotate(m[:, None, :], [p], rope["theta_s"])[:, 0, :]
             x += (float(num[e]) / float(den[j])) * m.reshape(-1)
+        if inv_r is not None:
+            x = x * float(np.asarray(inv_r, np.float64)[layer, role])
         xs[n] = x
         y = A_lc @ x
         if b_lc is not None:
             y = y + np.asarray(b_lc, dtype=np.float64)
         y = y.reshape(H_r, d_h)
+        if role == K and k_norm is not None:
+            y = rms_norm(y, np.asarray(k_norm)[layer], eps)
         if rot:
             qpos = rope.get("pos0_r", 0) + int(j)
             y = _rope.rotate(y[:, None, :], [qpos], rope["theta_r"])[:, 0, :]
@@ -173,13 +202,14 @@ def features_taps(S, taps, csr, rope, layer, role):
                            for t in np.asarray(taps)[layer]], axis=1)
 
 
-def transfer_taps(S, taps, csr, A, b=None, rope=None, H_r=None):
+def transfer_taps(S, taps, csr, A, b=None, rope=None, H_r=None, opts=None):
     """Whole receiver cache with concatenated-feature maps.
 
     taps  int [L_R, n] sender layers of each receiver layer
     A     [L_R, 2, d_R, n * d_S];  b  [L_R, 2, d_R] or None
     other arguments and the result as in ``transfer``
     """
+    inv_r, k_norm, eps = _opts(opts)
     S = np.asarray(S, dtype=np.float64)
     A = np.asarray(A, dtype=np.float64)
     taps = np.asarray(taps)
@@ -192,10 +222,15 @@ def transfer_taps(S, taps, csr, A, b=None, rope=None, H_r=None):
     out = np.empty((L_r, 2, H_r, T_r, d_h), dtype=np.float64)
     for l in range(L_r):
         for c in (K, V):
-            y = features_taps(S, taps, csr, rope, l, c) @ A[l, c].T
+            x = features_taps(S, taps, csr, rope, l, c)
+            if inv_r is not None:
+                x = x * float(np.asarray(inv_r, np.float64)[l, c])
+            y = x @ A[l, c].T
             if b is not None:
                 y = y + np.asarray(b, dtype=np.float64)[l, c][None, :]
             y = y.reshape(T_r, H_r, d_h).transpose(1, 0, 2)
+            if c == K and k_norm is not None:
+                y = rms_norm(y, np.asarray(k_norm)[l], eps)
             if c == K and rope is not None and rope.get("rotate_receiver_k", False):
                 y = _rope.rotate(y, rope.get("pos0_r", 0) + np.arange(T_r), rope["theta_r"])
             out[l, c] = y
@@ -203,9 +238,10 @@ def transfer_taps(S, taps, csr, A, b=None, rope=None, H_r=None):
 
 
 def transfer_rows_taps(get_sender, taps, csr, A_lc, b_lc, rope, d_h, layer, role, rows,
-                       return_features=False):
+                       return_features=False, opts=None):
     """Selected receiver rows of one (layer, role) with concatenated-feature
     maps, entry by entry (get_sender as in ``transfer_rows``)."""
+    inv_r, k_norm, eps = _opts(opts)
     taps = np.asarray(taps)[layer]
     row_ptr, col, num, den = (np.asarray(t, dtype=np.int64) for t in csr)
     A_lc = np.asarray(A_lc, dtype=np.float64)
@@ -231,11 +267,15 @@ def transfer_rows_taps(get_sender, taps, csr, A_lc, b_lc, rope, d_h, layer, role
                 x += (float(num[e]) / float(den[j])) * m.reshape(-1)
             blocks.append(x)
         x = np.concatenate(blocks)
+        if inv_r is not None:
+            x = x * float(np.asarray(inv_r, np.float64)[layer, role])
         xs[n] = x
         y = A_lc @ x
         if b_lc is not None:
             y = y + np.asarray(b_lc, dtype=np.float64)
         y = y.reshape(H_r, d_h)
+        if role == K and k_norm is not None:
+            y = rms_norm(y, np.asarray(k_norm)[layer], eps)
         if rot:
             qpos = rope.get("pos0_r", 0) + int(j)
             y = _rope.rotate(y[:, None, :], [qpos], rope["theta_r"])[:, 0, :]
