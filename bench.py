@@ -108,11 +108,17 @@ def cpu_baseline(wl, budget_s=30.0):
         A = wl.A[layer:layer + 1].float().cpu().numpy().astype(np.float64)
         bias = wl.bias[layer:layer + 1].float().cpu().numpy().astype(np.float64)
         rp = None if wl.rope is None else dict(wl.rope, pos0_s=0, pos0_r=0)
+        opts = None
+        if wl.opts is not None:
+            opts = dict(inv_r=wl.opts["inv_r"][layer:layer + 1].cpu().numpy().astype(np.float64),
+                        k_norm=wl.opts["k_norm"][layer:layer + 1].cpu().numpy().astype(np.float64),
+                        k_norm_eps=wl.opts["k_norm_eps"])
         if cfg.layer_map == "neighbor3":
             taps = lm.neighbor3(cfg.L_s, cfg.L_r)[layer]
             S = wl.S[b, list(taps), :, :, :T_s, :].float().cpu().numpy().astype(np.float64)
             t0 = time.perf_counter()
-            tr.transfer_taps(S, np.arange(len(taps))[None, :], csr[b], A, bias, rp, H_r=cfg.H_r)
+            tr.transfer_taps(S, np.arange(len(taps))[None, :], csr[b], A, bias, rp, H_r=cfg.H_r,
+                             opts=opts)
         else:
             lt = lm.interp2(cfg.L_s, cfg.L_r)
             lo, hi = int(lt[0][layer]), int(lt[1][layer])
@@ -121,7 +127,7 @@ def cpu_baseline(wl, budget_s=30.0):
             taps = [lo] if hi == lo else [lo, hi]
             S = wl.S[b, taps, :, :, :T_s, :].float().cpu().numpy().astype(np.float64)
             t0 = time.perf_counter()
-            tr.transfer(S, sub, csr[b], A, bias, rp, H_r=cfg.H_r)
+            tr.transfer(S, sub, csr[b], A, bias, rp, H_r=cfg.H_r, opts=opts)
         t_layer += time.perf_counter() - t0
         del S
     est = t_align + cfg.L_r * t_layer
@@ -168,7 +174,7 @@ def main():
     log(f"[bench] workload {cfg.name}: generating inputs on the GPU")
     wl = synth.make_workload(cfg, seed=args.seed, device="cuda")
     path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r,
-                        layer_map=cfg.layer_map)
+                        layer_map=cfg.layer_map, opts=wl.opts)
     torch.cuda.synchronize()
     T_r = int(wl.seg.r_len.sum())
     T_s = int(wl.seg.s_len.sum())
@@ -228,7 +234,9 @@ def main():
         "config": {"workload": cfg.name, "batch": wl.seg.batch, "T_s": T_s, "T_r": T_r,
                    "L_s": cfg.L_s, "L_r": cfg.L_r, "H_s": cfg.H_s, "H_r": cfg.H_r, "d_h": cfg.d_h,
                    "rope": list(cfg.rope) if cfg.rope else None, "alignment": "overlap",
-                   "layer_map": cfg.layer_map, "parallelism": "single-gpu"},
+                   "layer_map": cfg.layer_map,
+                   "sender_keys": "post-rope" if cfg.sender_keys_post_rope else "pre-rope",
+                   "inv_r_and_key_norm": bool(cfg.paper_opts), "parallelism": "single-gpu"},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

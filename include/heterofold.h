@@ -69,6 +69,27 @@ typedef enum { HF_ALIGN_OVERLAP = 0, HF_ALIGN_TA = 1 } hf_align_mode;
 typedef enum { HF_LAYERS_INTERP2 = 0 } hf_layer_mode;
 typedef enum { HF_F32 = 0, HF_BF16 = 1 } hf_dtype;
 
+/*
+ * Optional parts of the paper's cache construction for hf_transfer_kv and
+ * hf_transfer_kv_taps (pass NULL for none of them):
+ *   inv_r      device fp32 [L_r][2] or NULL: the scalar 1/r of Eq. 3 per
+ *              receiver layer and role; the map sees x_j / r (Eq. 9).  The
+ *              scaling happens in fp32 before x_j is rounded.  NULL: 1 (r
+ *              folded into A by the caller).
+ *   k_norm     device fp32 [L_r][d_h] or NULL: the receiver's key
+ *              normalization (App. B.1: mapped keys go through the receiver's
+ *              own key normalization, then its RoPE).  Per receiver head of
+ *              d_h features: y <- y / sqrt(mean(y^2) + k_norm_eps) * k_norm[l],
+ *              after the bias and before the receiver rotation.  Keys only.
+ *   k_norm_eps epsilon under the root, finite and >= 0.
+ * Buffers are caller-owned and 4-byte aligned.
+ */
+typedef struct {
+  const float* inv_r;
+  const float* k_norm;
+  float k_norm_eps;
+} hf_transfer_opts;
+
 /* Thread-local text of the last failure of a call made on this thread. */
 const char* hf_last_error(void);
 int32_t hf_version(void);
@@ -220,8 +241,9 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  *   m_i = a_lo S[lo_l, c, :, i, :] + a_hi S[hi_l, c, :, i, :]      (layer map)
  *   u_i = U_s(pos0_s + i) m_i  for keys when rope->unrotate_sender_k, else m_i
  *   x_j = sum over row j of (num/den_j) u_i, flattened head-major   (alignment)
- *   y_j = A[l, c] x_j + bias[l, c]                                  (Eq. 9)
- *   keys: y_j <- R_r(pos0_r + j) y_j per receiver head when rotate_receiver_k
+ *   y_j = A[l, c] (x_j * inv_r[l, c]) + bias[l, c]                  (Eq. 9)
+ *   keys: RMSNorm per receiver head when opts->k_norm (App. B.1), then
+ *         y_j <- R_r(pos0_r + j) y_j per receiver head when rotate_receiver_k
  *   R[l, c, h', j, e'] = y_j[h'*d_h + e']
  * Arguments
  *   s_len, r_len   host int32 [B]: token counts (<= sender/receiver T_cap).
@@ -233,6 +255,7 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  *   A_packed       device: maps packed by hf_pack_maps (same L_r, d_r, d_in, dtype).
  *   bias           device fp32 [L_r][2][d_r], or NULL for zero bias.
  *   rope           NULL = no RoPE.
+ *   opts           NULL, or the optional 1/r and key normalization (above).
  *   workspace      device, >= hf_transfer_workspace_bytes(), 256-B aligned.
  * Numerics: HF_F32 computes in fp32 throughout.  HF_BF16 forms x_j in fp32,
  * rounds it once to bf16 (round-to-nearest-even), multiplies on the matrix
@@ -247,8 +270,8 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
                        const int32_t* den, const int32_t* lo, const int32_t* hi,
                        const int32_t* rem, const int32_t* den_l, const hf_kv_desc* sender,
                        const hf_kv_desc* receiver, const void* A_packed, const float* bias,
-                       const hf_rope* rope, void* workspace, size_t workspace_bytes,
-                       void* stream);
+                       const hf_rope* rope, const hf_transfer_opts* opts, void* workspace,
+                       size_t workspace_bytes, void* stream);
 
 /*
  * hf_transfer_kv for maps over concatenated sender layers (Sec. 3.1 Eq. 2,
@@ -271,7 +294,8 @@ int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_le
                             const int32_t* den, int32_t n_taps, const int32_t* taps,
                             const hf_kv_desc* sender, const hf_kv_desc* receiver,
                             const void* A_packed, const float* bias, const hf_rope* rope,
-                            void* workspace, size_t workspace_bytes, void* stream);
+                            const hf_transfer_opts* opts, void* workspace,
+                            size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Kernel timing (tracing).                                                  */

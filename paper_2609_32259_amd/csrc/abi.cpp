@@ -386,8 +386,8 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
                       const int32_t* row_ptr, const int32_t* col, const int32_t* num,
                       const int32_t* den, const LayerSpec& ls, const hf_kv_desc* sender,
                       const hf_kv_desc* receiver, const void* A_packed, const float* bias,
-                      const hf_rope* rope, void* workspace, size_t workspace_bytes,
-                      void* stream) {
+                      const hf_rope* rope, const hf_transfer_opts* opts, void* workspace,
+                      size_t workspace_bytes, void* stream) {
   if (B < 1 || B > HF_MAX_BATCH) return fail(HF_ERR_SHAPE, "B=%d outside [1, %d]", B, HF_MAX_BATCH);
   if (!s_len || !r_len) return fail(HF_ERR_NULL, "s_len / r_len is NULL");
   if (ls.concat) {
@@ -445,6 +445,15 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
   if (rope && (!(rope->theta_s > 0) || !(rope->theta_r > 0) || !std::isfinite(rope->theta_s) ||
                !std::isfinite(rope->theta_r)))
     return fail(HF_ERR_SHAPE, "RoPE thetas must be finite and > 0");
+  if (opts) {
+    if ((opts->inv_r && (reinterpret_cast<uintptr_t>(opts->inv_r) & 3u)) ||
+        (opts->k_norm && (reinterpret_cast<uintptr_t>(opts->k_norm) & 3u)))
+      return fail(HF_ERR_SHAPE, "opts buffers must be 4-byte aligned");
+    if (opts->k_norm && !(std::isfinite(opts->k_norm_eps) && opts->k_norm_eps >= 0.0f))
+      return fail(HF_ERR_SHAPE, "k_norm_eps must be finite and >= 0");
+    if (opts->k_norm && dtype == HF_F32 && d_h != 64 && d_h != 128)
+      return fail(HF_ERR_UNSUPPORTED, "fp32 key normalization needs d_h in {64, 128}");
+  }
   RopeSizes rs;
   if ((st = rope_sizes(B, s_len, r_len, rope, rs))) return st;
   const size_t ws_need = rope_bytes(rs.P_s, d_h) + rope_bytes(rs.P_r, d_h);
@@ -462,6 +471,11 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
   a.R = receiver->ptr;
   a.Wp = A_packed;
   a.bias = bias;
+  if (opts) {
+    a.inv_r = opts->inv_r;
+    a.k_norm = opts->k_norm;
+    a.k_norm_eps = opts->k_norm_eps;
+  }
   a.row_ptr = row_ptr;
   a.col = col;
   a.num = num;
@@ -547,15 +561,15 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
                        const int32_t* den, const int32_t* lo, const int32_t* hi,
                        const int32_t* rem, const int32_t* den_l, const hf_kv_desc* sender,
                        const hf_kv_desc* receiver, const void* A_packed, const float* bias,
-                       const hf_rope* rope, void* workspace, size_t workspace_bytes,
-                       void* stream) {
+                       const hf_rope* rope, const hf_transfer_opts* opts, void* workspace,
+                       size_t workspace_bytes, void* stream) {
   LayerSpec ls;
   ls.lo = lo;
   ls.hi = hi;
   ls.rem = rem;
   ls.den_l = den_l;
   return transfer_impl(B, s_len, r_len, row_ptr, col, num, den, ls, sender, receiver, A_packed,
-                       bias, rope, workspace, workspace_bytes, stream);
+                       bias, rope, opts, workspace, workspace_bytes, stream);
 }
 
 int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_len,
@@ -563,13 +577,14 @@ int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_le
                             const int32_t* den, int32_t n_taps, const int32_t* taps,
                             const hf_kv_desc* sender, const hf_kv_desc* receiver,
                             const void* A_packed, const float* bias, const hf_rope* rope,
-                            void* workspace, size_t workspace_bytes, void* stream) {
+                            const hf_transfer_opts* opts, void* workspace,
+                            size_t workspace_bytes, void* stream) {
   LayerSpec ls;
   ls.concat = true;
   ls.n_taps = n_taps;
   ls.taps = taps;
   return transfer_impl(B, s_len, r_len, row_ptr, col, num, den, ls, sender, receiver, A_packed,
-                       bias, rope, workspace, workspace_bytes, stream);
+                       bias, rope, opts, workspace, workspace_bytes, stream);
 }
 
 int32_t hf_profiler_enable(int32_t on) {

@@ -52,6 +52,9 @@ struct TransferArgs {
   const int32_t* den;
   const float* cs_s;    // sender RoPE table [P_s][d_h]: cos of the d_h/2 angles, then sin
   const float* cs_r;    // receiver RoPE table [P_r][d_h], same layout
+  const float* inv_r;   // [L_r][2] scalar 1/r per layer and role, or nullptr (1)
+  const float* k_norm;  // [L_r][d_h] receiver key RMSNorm weights, or nullptr
+  float k_norm_eps;
   long long s_sb, s_sl, s_sc, s_sh, s_st;
   long long r_sb, r_sl, r_sc, r_sh, r_st;
   int32_t L_r, H_s, H_r, d_h;

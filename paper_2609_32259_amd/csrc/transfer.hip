@@ -139,6 +139,11 @@ __device__ __forceinline__ Ctx make_ctx(const TransferArgs& p, const Item& it, i
   x.wlo = p.concat ? 1.0f : p.wlo[it.l];
   x.whi = p.concat ? 0.0f : p.whi[it.l];
   x.two_tap = x.whi != 0.0f;
+  if (p.inv_r) {  // the map sees x / r: scale the layer weights
+    const float s = p.inv_r[it.l * 2 + it.c];
+    x.wlo *= s;
+    x.whi *= s;
+  }
   x.Ts = p.Ts[it.b];
   return x;
 }
@@ -195,6 +200,29 @@ __device__ __forceinline__ void build_row_global(const TransferArgs& p, const Ct
   }
 }
 
+// 1 / sqrt(mean(y^2) + eps) of one receiver head row of 128 features whose
+// squares are split between this lane (ss) and lane ^ 32.
+__device__ __forceinline__ float rms_scale_pair(float ss, float eps) {
+  ss += __shfl_xor(ss, 32);
+  return 1.0f / sqrtf(ss * (1.0f / kDH) + eps);
+}
+
+// y[q][4 g + u] *= inv * weight of its feature feat[q] + 8 g + hi4 + u.
+template <int NTW>
+__device__ __forceinline__ void scale_by_weights(float (*y)[16], const int* feat, int hi4,
+                                                 const float* wrow, float inv) {
+#pragma unroll
+  for (int q = 0; q < NTW; ++q)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const float4 w = *reinterpret_cast<const float4*>(wrow + feat[q] + 8 * g + hi4);
+      y[q][4 * g + 0] *= inv * w.x;
+      y[q][4 * g + 1] *= inv * w.y;
+      y[q][4 * g + 2] *= inv * w.z;
+      y[q][4 * g + 3] *= inv * w.w;
+    }
+}
+
 // Epilogue of one 32-row block of a wave: bias, receiver RoPE on keys, bf16
 // rounding, then a write through the wave's LDS staging rows so that global
 // stores cover whole contiguous row segments.
@@ -204,8 +232,9 @@ __device__ __forceinline__ void build_row_global(const TransferArgs& p, const Ct
 template <int NTW>
 __device__ __forceinline__ void epilogue_rows(const TransferArgs& p, f32x16* acc, const int* feat,
                                               const float* bias_head, const float* cr, bool rot,
-                                              uint16_t* stage, uint16_t* dst_head, int row_base,
-                                              int Tr, int lane) {
+                                              const float* knorm, uint16_t* stage,
+                                              uint16_t* dst_head, int row_base, int Tr, int lane) {
+  static_assert(NTW == 4, "the key norm needs the whole head in the wave");
   const int hi4 = 4 * (lane >> 5);
   const int mcol = lane & 31;
   const int j = row_base + mcol;
@@ -221,6 +250,14 @@ __device__ __forceinline__ void epilogue_rows(const TransferArgs& p, f32x16* acc
       y[q][4 * g + 2] = acc[q][4 * g + 2] + bv.z;
       y[q][4 * g + 3] = acc[q][4 * g + 3] + bv.w;
     }
+  if (knorm) {  // receiver key RMSNorm over the head's 128 features (lanes l, l ^ 32)
+    float ss = 0.0f;
+#pragma unroll
+    for (int q = 0; q < NTW; ++q)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) ss = fmaf(y[q][i], y[q][i], ss);
+    scale_by_weights<NTW>(y, feat, hi4, knorm, rms_scale_pair(ss, p.k_norm_eps));
+  }
   if (rot && j < Tr) {
     const float* crow = cr + (long long)j * kDH;
 #pragma unroll
@@ -311,7 +348,8 @@ constexpr int kSmemBytes = kOffEnt + kEntInts * 4;
 constexpr int kOffRcs = 0;                           // [64][cos 64 | sin 64] fp32
 constexpr int kOffBias = kOffRcs + 64 * kDH * 4;     // [d_r <= 1024] fp32
 constexpr int kOffStage = kOffBias + 1024 * 4;       // 8 waves x [32][kXS] bf16
-static_assert(kOffStage + 8 * 32 * kXS * 2 <= kXBytes, "store phase must fit the X region");
+constexpr int kOffRsum = kOffStage + 8 * 32 * kXS * 2;  // 8 waves x 32 fp32
+static_assert(kOffRsum + 8 * 32 * 4 <= kXBytes, "store phase must fit the X region");
 static_assert(kSmemBytes <= 160 * 1024, "LDS budget");
 
 // Group-walk build.  Wave w builds sender head w / WPH for 8 RPG consecutive
@@ -687,6 +725,8 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   uint16_t* stage = reinterpret_cast<uint16_t*>(smem + kOffStage) + wave * 32 * kXS;
   uint16_t* dst_head = static_cast<uint16_t*>(p.R) + it.b * p.r_sb + (long long)it.l * p.r_sl +
                        it.c * p.r_sc + head * p.r_sh;
+  float* rsum = reinterpret_cast<float*>(smem + kOffRsum);  // [8 waves][32] row sums of squares
+  const float* knorm = (it.c == 0 && p.k_norm) ? p.k_norm + (long long)it.l * kDH : nullptr;
   const int hi4 = 4 * (lane >> 5);
   const int mcol = lane & 31;
 #pragma unroll
@@ -704,6 +744,22 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
         y[q][4 * g + 2] = acc[mt][q][4 * g + 2] + bv.z;
         y[q][4 * g + 3] = acc[mt][q][4 * g + 3] + bv.w;
       }
+    if (knorm) {  // receiver key RMSNorm over each head's 128 features
+      float ss = 0.0f;
+#pragma unroll
+      for (int q = 0; q < NTW; ++q)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) ss = fmaf(y[q][i], y[q][i], ss);
+      ss += __shfl_xor(ss, 32);  // lane ^ 32 holds the same row's other features
+      if (NTW == 2) {            // the other half of the head sits in wave ^ 1
+        rsum[wave * 32 + mcol] = ss;
+        __syncthreads();
+        ss += rsum[(wave ^ 1) * 32 + mcol];
+        __syncthreads();
+      }
+      const float inv = 1.0f / sqrtf(ss * (1.0f / kDH) + p.k_norm_eps);
+      scale_by_weights<NTW>(y, feat, hi4, knorm, inv);
+    }
     if (rot) {
       const float4* crow = reinterpret_cast<const float4*>(rcs) + rl * 32;
 #pragma unroll
@@ -823,9 +879,10 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_direct_kernel(const Tran
   const float* bias_head = p.bias ? p.bias + (long long)lc_store * NB * 32 + wn * kDH : nullptr;
   const bool rot = it.c == 0 && p.rot;
   const float* cr = rot ? p.cs_r + (long long)p.pos0_r[it.b] * kDH : nullptr;
+  const float* knorm = (it.c == 0 && p.k_norm) ? p.k_norm + (long long)it.l * kDH : nullptr;
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt)
-    epilogue_rows<4>(p, acc[mt], feat, bias_head, cr, rot, stage, dst_head,
+    epilogue_rows<4>(p, acc[mt], feat, bias_head, cr, rot, knorm, stage, dst_head,
                      j0 + 64 * wm + 32 * mt, Tr, lane);
 }
 
@@ -846,8 +903,9 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
   const int Tr = p.Tr[it.b], Ts = p.Ts[it.b];
   const bool keys = it.c == 0;
   const bool unrot = keys && p.unrot, rot = keys && p.rot;
-  const float wlo = p.wlo[it.l], whi = p.whi[it.l];
-  const bool two_tap = whi != 0.0f;
+  const float sr = p.inv_r ? p.inv_r[it.l * 2 + it.c] : 1.0f;  // the map sees x / r
+  const float wlo = p.wlo[it.l] * sr, whi = p.whi[it.l] * sr;
+  const bool two_tap = p.whi[it.l] != 0.0f;
   const float* Sb = static_cast<const float*>(p.S) + it.b * p.s_sb + it.c * p.s_sc;
   const int lc_store = it.l * 2 + it.c;
 
@@ -893,15 +951,21 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
   const float* W = static_cast<const float*>(p.Wp) + (long long)lc_store * d_r * d_in;
   float* Rb = static_cast<float*>(p.R) + it.b * p.r_sb + (long long)it.l * p.r_sl + it.c * p.r_sc;
   constexpr int kMaxRT = 16;
-  for (int pc = threadIdx.x; pc < p.H_r * half; pc += kF32Threads) {
-    const int hr = pc / half, f = pc - hr * half;
+  const float* knorm = (keys && p.k_norm) ? p.k_norm + (long long)it.l * d : nullptr;
+  // Every thread takes the same number of trips (pc past the end computes
+  // nothing and stores nothing), so the key norm's shuffles see whole waves;
+  // the half = d/2 threads of one receiver head are consecutive lanes.
+  for (int pc0 = 0; pc0 < p.H_r * half; pc0 += kF32Threads) {
+    const int pc = pc0 + threadIdx.x;
+    const bool live = pc < p.H_r * half;
+    const int hr = live ? pc / half : 0, f = live ? pc - hr * half : 0;
     const int n1 = hr * d + f, n2 = n1 + half;
     float y1[kMaxRT], y2[kMaxRT];
 #pragma unroll
     for (int r = 0; r < kMaxRT; ++r) y1[r] = y2[r] = 0.f;
     const float* W1 = W + (long long)n1 * d_in;
     const float* W2 = W + (long long)n2 * d_in;
-    for (int k = 0; k < d_in; ++k) {
+    for (int k = 0; k < (live ? d_in : 0); ++k) {
       const float a1 = W1[k], a2 = W2[k];
 #pragma unroll
       for (int r = 0; r < kMaxRT; ++r) {
@@ -912,13 +976,22 @@ __global__ __launch_bounds__(kF32Threads) void transfer_f32_kernel(const Transfe
         }
       }
     }
-    const float b1 = p.bias ? p.bias[(long long)lc_store * d_r + n1] : 0.f;
-    const float b2 = p.bias ? p.bias[(long long)lc_store * d_r + n2] : 0.f;
+    const float b1 = (p.bias && live) ? p.bias[(long long)lc_store * d_r + n1] : 0.f;
+    const float b2 = (p.bias && live) ? p.bias[(long long)lc_store * d_r + n2] : 0.f;
+    const float g1 = knorm ? knorm[f] : 1.f, g2 = knorm ? knorm[f + half] : 1.f;
 #pragma unroll
     for (int r = 0; r < kMaxRT; ++r) {
       const int j = j0 + r;
-      if (r >= RT || j >= Tr) continue;
+      if (r >= RT) continue;  // uniform: the shuffles below stay whole-wave
       float v1 = y1[r] + b1, v2 = y2[r] + b2;
+      if (knorm) {  // RMSNorm over the head's d features, held by half lanes
+        float ss = fmaf(v1, v1, v2 * v2);
+        for (int o = 1; o < half; o <<= 1) ss += __shfl_xor(ss, o);
+        const float inv = 1.0f / sqrtf(ss / (float)d + p.k_norm_eps);
+        v1 *= inv * g1;
+        v2 *= inv * g2;
+      }
+      if (!live || j >= Tr) continue;
       if (rot) {
         const float* cs = p.cs_r + (long long)(p.pos0_r[it.b] + j) * d;
         const float c = cs[f], s = cs[half + f];

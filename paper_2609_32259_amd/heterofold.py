@@ -53,6 +53,10 @@ class hf_rope(C.Structure):
                 ("pos0_s", C.POINTER(C.c_int32)), ("pos0_r", C.POINTER(C.c_int32))]
 
 
+class hf_transfer_opts(C.Structure):
+    _fields_ = [("inv_r", C.c_void_p), ("k_norm", C.c_void_p), ("k_norm_eps", C.c_float)]
+
+
 _I32P = C.POINTER(C.c_int32)
 _SIGNATURES = {
     "hf_last_error": (C.c_char_p, []),
@@ -75,12 +79,13 @@ _SIGNATURES = {
     "hf_transfer_kv": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p, C.c_void_p,
                                    C.c_void_p, _I32P, _I32P, _I32P, _I32P,
                                    C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc), C.c_void_p,
-                                   C.c_void_p, C.POINTER(hf_rope), C.c_void_p, C.c_size_t,
-                                   C.c_void_p]),
+                                   C.c_void_p, C.POINTER(hf_rope), C.POINTER(hf_transfer_opts),
+                                   C.c_void_p, C.c_size_t, C.c_void_p]),
     "hf_transfer_kv_taps": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p,
                                         C.c_void_p, C.c_void_p, C.c_int32, _I32P,
                                         C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc), C.c_void_p,
-                                        C.c_void_p, C.POINTER(hf_rope), C.c_void_p, C.c_size_t,
+                                        C.c_void_p, C.POINTER(hf_rope),
+                                        C.POINTER(hf_transfer_opts), C.c_void_p, C.c_size_t,
                                         C.c_void_p]),
     "hf_profiler_enable": (C.c_int32, [C.c_int32]),
     "hf_profiler_reset": (C.c_int32, []),
@@ -299,6 +304,21 @@ def _rope_struct(rope):
                      rope.get("rotate_receiver_k", True), rope.get("pos0_s"), rope.get("pos0_r"))
 
 
+def _opts_struct(opts):
+    """opts: None or dict(inv_r=fp32 CUDA tensor [L_r, 2] or None,
+    k_norm=fp32 CUDA tensor [L_r, d_h] or None, k_norm_eps=float)."""
+    if opts is None:
+        return None
+    torch = _torch()
+    ptrs = []
+    for key in ("inv_r", "k_norm"):
+        t = opts.get(key)
+        if t is not None and (not t.is_cuda or t.dtype != torch.float32 or not t.is_contiguous()):
+            raise TypeError(f"{key} must be a contiguous fp32 CUDA tensor")
+        ptrs.append(C.c_void_p(t.data_ptr()) if t is not None else None)
+    return hf_transfer_opts(ptrs[0], ptrs[1], float(opts.get("k_norm_eps", 1e-6)))
+
+
 def hf_transfer_workspace_bytes(s_len, r_len, S, R, rope=None) -> int:
     s_len, r_len = _i32(s_len), _i32(r_len)
     sd, rd = kv_desc(S), kv_desc(R)
@@ -309,16 +329,18 @@ def hf_transfer_workspace_bytes(s_len, r_len, S, R, rope=None) -> int:
 
 
 def hf_transfer_kv(s_len, r_len, alignment: Alignment, layer_map, S, R, A_packed, bias=None,
-                   rope=None, workspace=None, stream=None):
+                   rope=None, workspace=None, stream=None, opts=None):
     """Map sender caches S [B, L_s, 2, H_s, T_cap, d_h] into receiver caches
     R [B, L_r, 2, H_r, T_cap, d_h] (written in place).  layer_map is the
     (lo, hi, rem, den) host table; rope a dict (theta_s, theta_r,
-    unrotate_sender_k, rotate_receiver_k, pos0_s, pos0_r) or None."""
+    unrotate_sender_k, rotate_receiver_k, pos0_s, pos0_r) or None; opts a
+    dict (inv_r, k_norm, k_norm_eps) or None."""
     torch = _torch()
     s_len, r_len = _i32(s_len), _i32(r_len)
     lo, hi, rem, den_l = (_i32(x) for x in layer_map)
     sd, rd = kv_desc(S), kv_desc(R)
     rs, keep = _rope_struct(rope)
+    os_ = _opts_struct(opts)
     wsb = hf_transfer_workspace_bytes(s_len, r_len, S, R, rope)
     if workspace is None and wsb > 0:
         workspace = torch.empty(wsb, dtype=torch.uint8, device=S.device)
@@ -331,6 +353,7 @@ def hf_transfer_kv(s_len, r_len, alignment: Alignment, layer_map, S, R, A_packed
         C.byref(sd), C.byref(rd), C.c_void_p(A_packed.data_ptr()),
         C.c_void_p(bias.data_ptr()) if bias is not None else None,
         C.byref(rs) if rs is not None else None,
+        C.byref(os_) if os_ is not None else None,
         C.c_void_p(workspace.data_ptr()) if workspace is not None else None,
         int(workspace.numel() * workspace.element_size()) if workspace is not None else 0,
         _stream(stream))
@@ -339,7 +362,7 @@ def hf_transfer_kv(s_len, r_len, alignment: Alignment, layer_map, S, R, A_packed
 
 
 def hf_transfer_kv_taps(s_len, r_len, alignment: Alignment, taps, S, R, A_packed, bias=None,
-                        rope=None, workspace=None, stream=None):
+                        rope=None, workspace=None, stream=None, opts=None):
     """hf_transfer_kv with concatenated-tap maps: taps is the host table
     [L_r, n_taps] (e.g. hf_build_layer_taps) and A_packed packs maps of input
     size n_taps * H_s * d_h."""
@@ -350,6 +373,7 @@ def hf_transfer_kv_taps(s_len, r_len, alignment: Alignment, taps, S, R, A_packed
         raise TypeError("taps must be a table [L_r, n_taps]")
     sd, rd = kv_desc(S), kv_desc(R)
     rs, keep = _rope_struct(rope)
+    os_ = _opts_struct(opts)
     wsb = hf_transfer_workspace_bytes(s_len, r_len, S, R, rope)
     if workspace is None and wsb > 0:
         workspace = torch.empty(wsb, dtype=torch.uint8, device=S.device)
@@ -362,6 +386,7 @@ def hf_transfer_kv_taps(s_len, r_len, alignment: Alignment, taps, S, R, A_packed
         C.byref(sd), C.byref(rd), C.c_void_p(A_packed.data_ptr()),
         C.c_void_p(bias.data_ptr()) if bias is not None else None,
         C.byref(rs) if rs is not None else None,
+        C.byref(os_) if os_ is not None else None,
         C.c_void_p(workspace.data_ptr()) if workspace is not None else None,
         int(workspace.numel() * workspace.element_size()) if workspace is not None else 0,
         _stream(stream))

@@ -19,13 +19,15 @@ from . import heterofold as hf
 
 class TransferPath:
     def __init__(self, seg, S, A, bias, rope: Optional[dict], L_r: int, H_r: int,
-                 mode: str = "overlap", R=None, pack_stream=None, layer_map: str = "interp2"):
+                 mode: str = "overlap", R=None, pack_stream=None, layer_map: str = "interp2",
+                 opts: Optional[dict] = None):
         import torch
 
         if layer_map not in ("interp2", "neighbor3"):
             raise ValueError(f"layer map {layer_map!r} unknown")
         self.torch = torch
         self.layer_mode = layer_map
+        self.opts = opts
         dev = S.device
         self.seg = seg
         self.mode = mode
@@ -81,10 +83,11 @@ class TransferPath:
         if self.layer_mode == "neighbor3":
             return hf.hf_transfer_kv_taps(self.s_len, self.r_len, self.alignment, self.layer_map,
                                           self.S, self.R, self.A_packed, self.bias, self.rope,
-                                          workspace=self.transfer_ws, stream=stream)
+                                          workspace=self.transfer_ws, stream=stream,
+                                          opts=self.opts)
         return hf.hf_transfer_kv(self.s_len, self.r_len, self.alignment, self.layer_map, self.S,
                                  self.R, self.A_packed, self.bias, self.rope,
-                                 workspace=self.transfer_ws, stream=stream)
+                                 workspace=self.transfer_ws, stream=stream, opts=self.opts)
 
     def step(self, stream=None):
         """One pass of the whole path (asynchronous on the stream)."""

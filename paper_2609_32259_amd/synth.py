@@ -51,6 +51,8 @@ class Config:
     rope: Optional[Tuple[float, float]] = None   # (theta_s, theta_r): keys stored post-RoPE
     batch: int = 1
     layer_map: str = "interp2"      # "interp2" or "neighbor3" (three concatenated sender layers)
+    sender_keys_post_rope: bool = True   # False: the payload's keys are pre-RoPE (no un-rotation)
+    paper_opts: bool = False        # draw 1/r per (layer, role) and receiver key-norm weights
 
     @property
     def d_in(self) -> int:
@@ -88,6 +90,11 @@ LLAMA8B_14B_32K = LLAMA8B_14B_8K.with_(name="llama8b->14b-shape T_s=32768 rope",
 # The same shape with the paper's three-layer neighbourhood map (A is d_r x 3 d_in).
 LLAMA8B_14B_32K_N3 = LLAMA8B_14B_32K.with_(name="llama8b->14b-shape T_s=32768 rope neighbor3",
                                            layer_map="neighbor3")
+# The paper's cache construction at that shape: three-layer map, pre-RoPE
+# sender keys, the map on x / r, the receiver's key norm, then its RoPE.
+LLAMA8B_14B_32K_PAPER = LLAMA8B_14B_32K_N3.with_(
+    name="llama8b->14b-shape T_s=32768 neighbor3 pre-rope 1/r knorm",
+    sender_keys_post_rope=False, paper_opts=True)
 # Qwen-7B -> Llama-8B shape (layer upsampling), batch of 4, theta 1e6 -> 5e5.
 QWEN7B_LLAMA8B_B4 = Config("qwen7b->llama8b-shape B=4 rope", "bf16", L_s=28, L_r=32, H_s=4,
                            H_r=8, d_h=128, T_s=4096, bias_var=0.05, rope=(1.0e6, 5.0e5),
@@ -99,6 +106,7 @@ CONFIGS = {
     "14b-8k": LLAMA8B_14B_8K,
     "14b-32k": LLAMA8B_14B_32K,
     "14b-32k-n3": LLAMA8B_14B_32K_N3,
+    "14b-32k-paper": LLAMA8B_14B_32K_PAPER,
     "reverse-b4": QWEN7B_LLAMA8B_B4,
 }
 
@@ -245,6 +253,7 @@ class Workload:
     A: "object"          # torch [L_r, 2, d_r, d_in], storage dtype
     bias: "object"       # torch fp32 [L_r, 2, d_r]
     rope: Optional[dict]
+    opts: Optional[dict] = None   # inv_r, k_norm, k_norm_eps (make_opts)
 
     @property
     def T_cap_s(self):
@@ -298,8 +307,22 @@ def rope_params(cfg: Config, pos0_s=None, pos0_r=None):
     if cfg.rope is None:
         return None
     return dict(theta_s=float(cfg.rope[0]), theta_r=float(cfg.rope[1]),
-                unrotate_sender_k=True, rotate_receiver_k=True,
+                unrotate_sender_k=bool(cfg.sender_keys_post_rope), rotate_receiver_k=True,
                 pos0_s=pos0_s, pos0_r=pos0_r)
+
+
+def make_opts(cfg: Config, seed: int = 0, device="cpu", eps: float = 1e-6):
+    """The paper-faithful options, or None: inv_r [L_r, 2] ~ 1 / U(0.8, 1.25)
+    and receiver key-norm weights [L_r, d_h] ~ U(0.5, 1.5), fp32, drawn from
+    the map stream after the maps."""
+    if not cfg.paper_opts:
+        return None
+    torch = _torch()
+    _, _, _, map_seq = _child_seeds(seed, 4)
+    g = _torch_gen(map_seq.spawn(1)[0], device)
+    r = 0.8 + 0.45 * torch.rand((cfg.L_r, 2), generator=g, dtype=torch.float32, device=device)
+    k_norm = 0.5 + torch.rand((cfg.L_r, cfg.d_h), generator=g, dtype=torch.float32, device=device)
+    return dict(inv_r=(1.0 / r).contiguous(), k_norm=k_norm, k_norm_eps=float(eps))
 
 
 def make_workload(cfg: Config, seed: int = 0, device="cpu", T_s: Optional[int] = None,
@@ -307,4 +330,4 @@ def make_workload(cfg: Config, seed: int = 0, device="cpu", T_s: Optional[int] =
     seg = make_segmentation(cfg, seed, T_s=T_s, batch=batch)
     S = make_cache(cfg, seg, seed, device)
     A, bias = make_maps(cfg, seed, device)
-    return Workload(cfg, seg, S, A, bias, rope_params(cfg))
+    return Workload(cfg, seg, S, A, bias, rope_params(cfg), make_opts(cfg, seed, device))

@@ -12,6 +12,11 @@ For that case ("quantization-limited") every element must satisfy
 two roundings the arithmetic performs,
     half_ulp(y) + sum_k |A_nk| half_ulp(x_k)   (+ an fp32 accumulation term),
 which a wrong index, sign or dropped term would exceed.
+Keys that go through the receiver's key normalization (RMSNorm per head,
+then RoPE) have |y| of several units, where the output's own half-ulp
+(1/64 at |y| in [4, 8)) again leaves little room under 2e-2.  They are
+gated the same way with the first-order bound carried through the norm and
+the rotation (``rounding_bound_normed``).
 fp32 outputs: the same gates, plus relative Frobenius error <= 1e-5.
 """
 
@@ -47,15 +52,43 @@ def rounding_bound(ref, x, A):
     return bf16_half_ulp(np.abs(ref) * (1 + 2.0 ** -7) + b) + b
 
 
-def check_layer(got, ref, where, dtype="bf16", quantization_limited=False, x=None, A=None):
+def rounding_bound_normed(ref, x, A, b, g, eps, rotated):
+    """First-order bound for keys y = R(q) norm(A x + b) with x and y rounded
+    to bf16.  ref [H_r, T, d_h] oracle outputs; x [T, d_S] oracle features
+    (as the map sees them, 1/r applied); A [d_R, d_S]; b [d_R] or None;
+    g [d_h] norm weights; eps; rotated: whether the receiver RoPE follows."""
+    H_r, T, d_h = ref.shape
+    Aa = np.abs(np.asarray(A, dtype=np.float64))
+    x = np.asarray(x, dtype=np.float64)
+    y = x @ np.asarray(A, dtype=np.float64).T
+    if b is not None:
+        y = y + np.asarray(b, dtype=np.float64)[None, :]
+    e = bf16_half_ulp(x) @ Aa.T + 1e-5 * (np.abs(x) @ Aa.T)          # error before the norm
+    y = y.reshape(T, H_r, d_h)
+    e = e.reshape(T, H_r, d_h)
+    rho = np.sqrt(np.mean(y * y, axis=-1, keepdims=True) + float(eps))
+    en = np.linalg.norm(e, axis=-1, keepdims=True)
+    gg = np.abs(np.asarray(g, dtype=np.float64))
+    e = gg * (e / rho + np.abs(y) * en / (np.sqrt(d_h) * rho * rho))  # through the RMSNorm
+    e = e + 1e-6 * gg * np.abs(y) / rho
+    if rotated:                                                       # pair mixing by RoPE
+        h = d_h // 2
+        e = np.concatenate([e[..., :h] + e[..., h:], e[..., :h] + e[..., h:]], axis=-1)
+    e = e.transpose(1, 0, 2)
+    return bf16_half_ulp(np.abs(ref) * (1 + 2.0 ** -7) + e) + e
+
+
+def check_layer(got, ref, where, dtype="bf16", quantization_limited=False, x=None, A=None,
+                bound=None):
     rel, mx, d = err_stats(got, ref)
     assert np.all(np.isfinite(got)), f"{where}: non-finite output"
     assert rel <= REL_FRO, f"{where}: rel Frobenius {rel:.3e} > {REL_FRO}"
     if dtype == "f32":
         assert rel <= 1e-5, f"{where}: fp32 rel Frobenius {rel:.3e} > 1e-5"
     if quantization_limited:
-        assert x is not None and A is not None, "quantization-limited gate needs x and A"
-        bound = rounding_bound(ref, x, A)
+        if bound is None:
+            assert x is not None and A is not None, "quantization-limited gate needs x and A"
+            bound = rounding_bound(ref, x, A)
         bad = (np.abs(d) > MAX_ABS) & (np.abs(d) > bound)
         assert not bad.any(), (f"{where}: {int(bad.sum())} elements beyond both 2e-2 and the "
                                f"rounding bound; worst |err| {mx:.3e}")

@@ -118,12 +118,13 @@ def test_transfer_host_validation(L):
     fake = C.c_void_p(0x1000)
 
     def call(sd=None, rd=None, B=1, sl=s_len, rl=r_len, table=lt, A=fake, rope=None, ws=None, wsb=0,
-             rp=fake):
+             rp=fake, opts=None):
         sd = sd or _desc()
         rd = rd or _desc(L_=6)
         return L.hf_transfer_kv(B, _p(sl), _p(rl), rp, fake, fake, fake, *[_p(t) for t in table],
                                 C.byref(sd), C.byref(rd), A, None,
-                                C.byref(rope) if rope is not None else None, ws, wsb, None)
+                                C.byref(rope) if rope is not None else None,
+                                C.byref(opts) if opts is not None else None, ws, wsb, None)
 
     assert call(B=0) == -2
     assert call(rp=None) == -1
@@ -145,6 +146,11 @@ def test_transfer_host_validation(L):
     assert call(rope=r) == -1                                  # RoPE needs a workspace
     r2, keep2 = hf.make_rope(-1.0, 1e9)
     assert call(rope=r2, ws=fake, wsb=1 << 30) == -2
+    assert call(opts=hf.hf_transfer_opts(None, C.c_void_p(0x1000), -1.0)) == -2      # eps < 0
+    assert call(opts=hf.hf_transfer_opts(None, C.c_void_p(0x1000), float("nan"))) == -2
+    assert call(opts=hf.hf_transfer_opts(C.c_void_p(0x1002), None, 0.0)) == -2      # misaligned
+    assert call(sd=_desc(dtype=0, d=96), rd=_desc(L_=6, dtype=0, d=96),
+                opts=hf.hf_transfer_opts(None, C.c_void_p(0x1000), 1e-6)) == -8   # fp32 norm d_h
     # cos/sin tables: 64 sender + 60 receiver positions x 64 pairs x 8 bytes
     assert L.hf_transfer_workspace_bytes(1, _p(s_len), _p(r_len), C.byref(_desc()),
                                          C.byref(_desc(L_=6)), C.byref(r)) == 64 * 512 + 60 * 512
@@ -196,7 +202,7 @@ def test_transfer_taps_host_validation(L):
         rd = rd or _desc(L_=6)
         return L.hf_transfer_kv_taps(1, _p(s_len), _p(r_len), fake, fake, fake, fake, n,
                                      _p(tp) if tp is not None else None, C.byref(sd),
-                                     C.byref(rd), fake, None, None, None, 0, None)
+                                     C.byref(rd), fake, None, None, None, None, 0, None)
 
     assert call(tp=None) == -1
     assert call(n=0) == -2
