@@ -16,9 +16,12 @@ Everything here is written to be checked against the paper by eye:
 * ``transfer``   -- the folded affine K/V map of Eq. 9 applied to the aligned,
   layer-interpolated sender cache, with RoPE un-rotation of post-RoPE sender
   keys and re-rotation at receiver positions.
+* ``recolor``    -- the offline construction of those maps: sender RMS (Eq. 3),
+  weighted moments, whitening + Procrustes (Eq. 4), Recolor (Eq. 5), and the
+  low-rank correction folded into the map (Eq. 9).
 
 Integer results are exact.  Floating-point results are fp64 computed from the
 exact stored input values (bf16 or fp32 widened to fp64).
 """
 
-from . import alignment, layer_map, rope, transfer  # noqa: F401
+from . import alignment, layer_map, recolor, rope, transfer  # noqa: F401
