@@ -11,6 +11,11 @@ with inputs already resident in HBM.  Prints ONE JSON line (rank 0):
             launch stream over the timed steps) against the MI355X dense bf16 peak
   cpu_baseline  the fp64 CPU oracle on a bounded sample of the same workload
 
+With --workload calib-14b (or calib-small) it times the offline construction
+of one map instead: hf_recolor_moments -> hf_recolor_solve -> hf_fold_map over
+2^20 synthetic calibration samples, value = samples/s, roofline = the fp64
+covariance product against the MI355X fp64 matrix-core peak.
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 """
 
@@ -30,6 +35,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0
+PEAK_FP64_TFLOPS = 78.6     # MI355X dense fp64 matrix-core peak
+CALIB_METRIC = "calibration samples/sec for one map (moments + Recolor + fold, fp64)"
 METRIC = "receiver KV tokens/sec (all layers, K+V) at 32K; % of MFMA/HBM roofline"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "transfer_bf16_14b_32k_traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_32259_amd", "csrc", "transfer.hip")
@@ -138,6 +145,121 @@ def cpu_baseline(wl, budget_s=30.0):
                        f"scaled to {cfg.L_r} layers: {est:.1f} s per step of {T_r} receiver tokens")}
 
 
+def cpu_baseline_calib(x, y, w, p, rank, budget_rows=16384):
+    """The fp64 oracle on the host: weighted moments of the first budget_rows
+    samples (scaled to all n) plus the Recolor solve and the fold on them."""
+    from oracle import recolor as rc
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    n = int(x.shape[0])
+    k = min(n, budget_rows)
+    X = x[:k].double().cpu().numpy()
+    Y = y[:k].double().cpu().numpy()
+    W = w[:k].double().cpu().numpy()
+    t0 = time.perf_counter()
+    r = rc.sender_rms(X, W)
+    mz, my, Szz, Szy, Syy = rc.weighted_moments(X / r, Y, W)
+    t_mom = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    A, b = rc.recolor(mz, my, Szz, Szy, Syy, 1e-6)
+    q = A.shape[1]
+    rng = np.random.default_rng(0)
+    rc.fold(A, b, 0.02 * rng.standard_normal((q, rank)), rng.standard_normal((rank, q)))
+    t_solve = time.perf_counter() - t0
+    est = t_mom * n / k + t_solve
+    return {"value": n / est, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"fp64 NumPy oracle: weighted moments of {k} samples ({t_mom:.2f} s, "
+                       f"scaled to {n}) + Recolor solve and rank-{rank} fold ({t_solve:.2f} s): "
+                       f"{est:.1f} s per map")}
+
+
+def run_calibration(args, cfg):
+    import torch
+    from paper_2609_32259_amd import heterofold as hf
+    from paper_2609_32259_amd import synth
+
+    rank, ridge = 16, 1e-6
+    log(f"[bench] workload {cfg.name}: generating samples on the GPU")
+    x, y, w = synth.make_calibration(cfg, seed=args.seed, device="cuda")
+    p, q, n = cfg.p, cfg.q, cfg.n
+    g = torch.Generator(device="cuda")
+    g.manual_seed(args.seed + 1)
+    B = 0.02 * torch.randn((q, rank), generator=g, dtype=torch.float64, device="cuda")
+    G = torch.randn((rank, q), generator=g, dtype=torch.float64, device="cuda")
+    ws_m = torch.empty(hf.hf_recolor_moments_workspace_bytes(n, p, q), dtype=torch.uint8,
+                       device="cuda")
+    ws_s = torch.empty(hf.hf_recolor_solve_workspace_bytes(p, q), dtype=torch.uint8,
+                       device="cuda")
+    ws_f = torch.empty(hf.hf_fold_workspace_bytes(p, rank), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+
+    def step():
+        r, mu, cov = hf.hf_recolor_moments(x, y, w, workspace=ws_m)
+        A, b, info = hf.hf_recolor_solve(mu, cov, p, ridge=ridge, workspace=ws_s)
+        hf.hf_fold_map(A, b, B, G, out=(A, b), workspace=ws_f)
+        return info
+
+    log(f"[bench] n={n} p={p} q={q}; warmup {args.warmup}")
+    info = None
+    for _ in range(args.warmup):
+        info = step()
+    torch.cuda.synchronize()
+    if info is not None:
+        log(f"[bench] solve convergence {hf.recolor_info(info)}")
+    hf.hf_profiler_reset()
+    hf.hf_profiler_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        info = step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    hf.hf_profiler_enable(False)
+    conv = hf.recolor_info(info)
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    parts = {}
+    for name, kid in (("stats", hf.HF_KERNEL_MOMENTS_STATS), ("cov", hf.HF_KERNEL_MOMENTS_COV),
+                      ("solve", hf.HF_KERNEL_RECOLOR_SOLVE), ("fold", hf.HF_KERNEL_FOLD)):
+        t, c = hf.hf_profiler_query(kid)
+        parts[name] = t / max(c, 1)
+    log(f"[bench] step {ms_step:.2f} ms; " + ", ".join(f"{k} {v:.2f} ms" for k, v in parts.items()))
+    m = p + q
+    flops = 2.0 * n * m * (m + 1) / 2   # distinct entries of the symmetric Gram product
+    achieved = flops / (parts["cov"] * 1e-3) / 1e12
+    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_FP64_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_FP64_TFLOPS, 4), "traffic": None,
+            "kernel": "gemm_f64_kernel<1, float, true, true>", "kernel_ms": round(parts["cov"], 3),
+            "stats_ms": round(parts["stats"], 3), "solve_ms": round(parts["solve"], 3),
+            "fold_ms": round(parts["fold"], 3)}
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a bounded sample")
+        cpu = cpu_baseline_calib(x, y, w, p, rank)
+    out = {
+        "metric": CALIB_METRIC,
+        "value": round(n / (ms_step * 1e-3), 1),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "n": n, "p": p, "q": q, "sample_dtype": cfg.dtype,
+                   "ridge": ridge, "rank": rank, "solve_converged": conv["converged"],
+                   "solve_iterations": conv["iterations"], "parallelism": "single-gpu"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -170,6 +292,9 @@ def main():
         torch.cuda.synchronize()
         log(f"[bench] copy probe: {args.copy_probe_mib} MiB read + {args.copy_probe_mib} MiB written")
         del src, dst
+    if args.workload in synth.CALIB_CONFIGS:
+        run_calibration(args, synth.CALIB_CONFIGS[args.workload])
+        return
     cfg = synth.CONFIGS[args.workload]
     log(f"[bench] workload {cfg.name}: generating inputs on the GPU")
     wl = synth.make_workload(cfg, seed=args.seed, device="cuda")

@@ -298,6 +298,120 @@ int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_le
                             size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Offline construction of the maps (fp64, off the transfer path).           */
+/* ------------------------------------------------------------------------ */
+/*
+ * For one receiver layer and role, N paired calibration samples x_n (aligned
+ * sender feature, p = d~_S values: the concatenated taps of Eq. 2) and y_n
+ * (receiver feature, q = d_R values) with weights w_n.  The three calls below
+ * give the folded map the transfer calls take:
+ *
+ *   hf_recolor_moments  r of Eq. 3, and the weighted means and joint
+ *                       covariance of [x/r | y] (Sec. 3.2);
+ *   hf_recolor_solve    Recolor (Eq. 4-5): A = S_Z^{-1/2} R* S_Y^{1/2},
+ *                       b = mu_Y - mu_Z A, R* = U Q^T from the thin SVD
+ *                       S_Z^{-1/2} S_ZY S_Y^{-1/2} = U Lambda Q^T;
+ *   hf_fold_map         the output-aware correction folded in (Eq. 9):
+ *                       A (I + B G), b (I + B G).
+ *
+ * Maps are returned in the transfer path's orientation: A stored [q][p]
+ * row-major (the paper's row-vector A transposed), so y = A (x/r) + b.  The
+ * caller converts A to the storage type of hf_pack_maps, b to the fp32 bias,
+ * and 1/r to hf_transfer_opts.inv_r (or folds 1/r into A).
+ *
+ * All arithmetic is fp64 (samples widened exactly).  Conventions as above:
+ * device pointers are caller-owned HIP memory, nothing is allocated, scratch
+ * comes from the workspace, work is enqueued on `stream` and no call
+ * synchronizes the host.
+ */
+
+/*
+ * Weighted sender RMS, means and joint covariance (Eq. 3; Sec. 3.2).
+ *   n          samples, >= 1.
+ *   p, q       feature sizes, each in [1, 65536].
+ *   dtype      HF_F32 or HF_BF16: storage of x and y.
+ *   x          device [n][ldx], row n holds x_n in its first p entries (ldx >= p).
+ *   y          device [n][ldy], y_n in the first q entries (ldy >= q).
+ *   w          device fp32 [n] sample weights (>= 0, positive sum), or NULL for 1.
+ *   r          device fp64 [1]: r = sqrt(sum w |x|^2 / (p sum w)).
+ *   mu         device fp64 [p + q]: weighted means of z = x / r, then of y.
+ *   cov        device fp64 [(p + q)^2] row-major: the joint covariance of
+ *              [z | y], normalized by sum w (blocks S_Z, S_ZY / S_YZ, S_Y).
+ *              Exactly symmetric.
+ *   workspace  device, >= hf_recolor_moments_workspace_bytes(n, p, q), 256-B aligned.
+ * The covariance is accumulated over centred samples (two passes).  A weight
+ * sum of zero gives NaN results.
+ */
+size_t hf_recolor_moments_workspace_bytes(int64_t n, int32_t p, int32_t q);
+int32_t hf_recolor_moments(int64_t n, int32_t p, int32_t q, int32_t dtype, const void* x,
+                           int64_t ldx, const void* y, int64_t ldy, const float* w, double* r,
+                           double* mu, double* cov, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* Convergence of the three Newton-Schulz iterations of hf_recolor_solve
+ * (index 0: roots of S_Z, 1: roots of S_Y, 2: the Procrustes factor). */
+typedef struct {
+  int32_t iterations[3];  /* steps taken */
+  int32_t converged[3];   /* 1: residual below 1e-3 and three more steps taken */
+  double residual[3];     /* last |I - P|_F (P = Z Y for the roots, X^T X or X X^T) */
+} hf_recolor_info;
+
+/*
+ * Recolor initialization from moments (Eq. 4-5).
+ *   p, q       as in hf_recolor_moments.
+ *   mu, cov    device fp64: hf_recolor_moments' outputs (or any means and SPD
+ *              joint covariance in that layout).
+ *   ridge      >= 0: S + ridge * (trace S / dim) * I replaces S_Z and S_Y
+ *              before their roots (the paper's numerical stabilization is
+ *              unspecified; 0 is the unregularized map).
+ *   A          device fp64 [q][p] (out).
+ *   b          device fp64 [q] (out).
+ *   info       device hf_recolor_info (out), or NULL.
+ *   workspace  device, >= hf_recolor_solve_workspace_bytes(p, q), 256-B aligned.
+ * Method: the symmetric roots S^{1/2}, S^{-1/2} by the coupled Newton-Schulz
+ * iteration after scaling S by its Frobenius norm; R* as the polar factor of
+ * the whitened cross-covariance by the Newton-Schulz polar iteration (equal to
+ * U Q^T when that matrix has full rank).  Each iteration stops three steps
+ * after its residual falls below 1e-3, or after 64 (roots) / 128 (polar)
+ * steps; the call returns before the device finishes, so read info after the
+ * stream completes: converged[i] == 0 means the result is not valid (a
+ * singular covariance without ridge, or a rank-deficient cross-covariance).
+ */
+size_t hf_recolor_solve_workspace_bytes(int32_t p, int32_t q);
+int32_t hf_recolor_solve(int32_t p, int32_t q, const double* mu, const double* cov, double ridge,
+                         double* A, double* b, hf_recolor_info* info, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/*
+ * Fold a rank-`rank` correction y^ = y0 + (y0 B) G into the map (Eq. 9):
+ * the paper's A (I + B G) and b (I + B G), in the stored orientation
+ * A_out = A + G^T (B^T A), b_out = b + G^T (B^T b).
+ *   A, b       device fp64 [q][p] and [q] (e.g. from hf_recolor_solve).
+ *   B          device fp64 [q][rank] (the paper's B, d_R x rho).
+ *   G          device fp64 [rank][q].
+ *   A_out, b_out  device fp64 [q][p], [q]; may be A and b themselves.
+ *   rank       >= 1.
+ *   workspace  device, >= hf_fold_workspace_bytes(p, rank), 256-B aligned.
+ */
+size_t hf_fold_workspace_bytes(int32_t p, int32_t rank);
+int32_t hf_fold_map(int32_t p, int32_t q, int32_t rank, const double* A, const double* b,
+                    const double* B, const double* G, double* A_out, double* b_out,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The fp64 matrix-core product behind the three calls above, exposed for
+ * testing and reuse: D = alpha * op(A) op(B) + beta * C + gamma * I, where
+ * op(A) is m x k, element (i, kk) at A[kk * lda + i] when a_kmajor else
+ * A[i * lda + kk], and op(B) is k x n, element (kk, j) at B[kk * ldb + j] when
+ * b_kmajor else B[j * ldb + kk].  D is [m][ldd] row-major; C (read only when
+ * beta != 0) is [m][ldc] and may be D.  m, n >= 1, k >= 0.
+ */
+int32_t hf_gemm_f64(int32_t m, int32_t n, int64_t k, const double* A, int64_t lda,
+                    int32_t a_kmajor, const double* B, int64_t ldb, int32_t b_kmajor, double* D,
+                    int64_t ldd, double alpha, double beta, const double* C, int64_t ldc,
+                    double gamma, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timing (tracing).                                                  */
 /* ------------------------------------------------------------------------ */
 
@@ -306,7 +420,11 @@ typedef enum {
   HF_KERNEL_ROPE_TABLES = 1,/* cos/sin table kernel of hf_transfer_kv */
   HF_KERNEL_ALIGNMENT = 2,  /* the three kernels of hf_build_alignment, together */
   HF_KERNEL_PACK = 3,       /* hf_pack_maps */
-  HF_KERNEL_COUNT = 4
+  HF_KERNEL_MOMENTS_STATS = 4, /* the column-statistics kernels of hf_recolor_moments */
+  HF_KERNEL_MOMENTS_COV = 5,   /* the covariance product of hf_recolor_moments */
+  HF_KERNEL_RECOLOR_SOLVE = 6, /* all launches of hf_recolor_solve */
+  HF_KERNEL_FOLD = 7,          /* all launches of hf_fold_map */
+  HF_KERNEL_COUNT = 8
 } hf_kernel_id;
 
 /*

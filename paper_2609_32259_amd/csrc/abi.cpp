@@ -587,6 +587,160 @@ int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_le
                        bias, rope, opts, workspace, workspace_bytes, stream);
 }
 
+// ---------------------------------------------------------------------------
+// Offline map construction.
+// ---------------------------------------------------------------------------
+
+size_t hf_recolor_moments_workspace_bytes(int64_t n, int32_t p, int32_t q) {
+  if (n < 1 || p < 1 || q < 1) return 0;
+  return hf::recolor_moments_workspace_bytes(n, p, q);
+}
+
+size_t hf_recolor_solve_workspace_bytes(int32_t p, int32_t q) {
+  if (p < 1 || q < 1) return 0;
+  return hf::recolor_solve_workspace_bytes(p, q);
+}
+
+size_t hf_fold_workspace_bytes(int32_t p, int32_t rank) {
+  if (p < 1 || rank < 1) return 0;
+  return hf::fold_workspace_bytes(p, rank);
+}
+
+namespace {
+
+constexpr int32_t kMaxFeatures = 65536;
+constexpr int64_t kMaxGemmRows = 65535LL * 64;  // row tiles of 64 on the grid's y axis
+
+bool aligned_to(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const char* x = static_cast<const char*>(a);
+  const char* y = static_cast<const char*>(b);
+  return x < y + nb && y < x + na;
+}
+
+int32_t check_workspace(const void* ws, size_t bytes, size_t need) {
+  if (!ws) return fail(HF_ERR_NULL, "workspace is NULL");
+  if (!aligned_to(ws, 256)) return fail(HF_ERR_SHAPE, "workspace is not 256-byte aligned");
+  if (bytes < need) return fail(HF_ERR_CAPACITY, "workspace %zu bytes < required %zu", bytes, need);
+  return HF_OK;
+}
+
+}  // namespace
+
+int32_t hf_recolor_moments(int64_t n, int32_t p, int32_t q, int32_t dtype, const void* x,
+                           int64_t ldx, const void* y, int64_t ldy, const float* w, double* r,
+                           double* mu, double* cov, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  if (n < 1) return fail(HF_ERR_SHAPE, "need n >= 1 samples");
+  if (p < 1 || q < 1 || p > kMaxFeatures || q > kMaxFeatures || p + q > kMaxFeatures)
+    return fail(HF_ERR_SHAPE, "need p, q >= 1 and p + q <= %d", kMaxFeatures);
+  if (dtype != HF_F32 && dtype != HF_BF16) return fail(HF_ERR_DTYPE, "dtype %d unknown", dtype);
+  if (!x || !y || !r || !mu || !cov) return fail(HF_ERR_NULL, "x / y / r / mu / cov is NULL");
+  if (ldx < p || ldy < q) return fail(HF_ERR_SHAPE, "need ldx >= p and ldy >= q");
+  const size_t es = dtype == HF_BF16 ? 2 : 4;
+  if (!aligned_to(x, es) || !aligned_to(y, es) || (w && !aligned_to(w, 4)))
+    return fail(HF_ERR_SHAPE, "x / y / w not aligned to their element size");
+  if (!aligned_to(r, 8) || !aligned_to(mu, 8) || !aligned_to(cov, 8))
+    return fail(HF_ERR_SHAPE, "r / mu / cov not 8-byte aligned");
+  const size_t pq = (size_t)p + q;
+  if (overlap(cov, pq * pq * 8, mu, pq * 8) || overlap(cov, pq * pq * 8, r, 8) ||
+      overlap(mu, pq * 8, r, 8))
+    return fail(HF_ERR_SHAPE, "r, mu and cov overlap");
+  int32_t st;
+  if ((st = check_workspace(workspace, workspace_bytes, hf::recolor_moments_workspace_bytes(n, p, q))))
+    return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    TimedLaunch t(HF_KERNEL_MOMENTS_STATS, s);
+    e = hf::launch_recolor_stats(dtype, n, p, q, x, ldx, y, ldy, w, r, mu, workspace, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "moments statistics launch");
+  {
+    TimedLaunch t(HF_KERNEL_MOMENTS_COV, s);
+    e = hf::launch_recolor_cov(dtype, n, p, q, x, ldx, y, ldy, w, cov, workspace, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "covariance launch");
+  return ok();
+}
+
+int32_t hf_recolor_solve(int32_t p, int32_t q, const double* mu, const double* cov, double ridge,
+                         double* A, double* b, hf_recolor_info* info, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  if (p < 1 || q < 1 || p > kMaxFeatures || q > kMaxFeatures || p + q > kMaxFeatures)
+    return fail(HF_ERR_SHAPE, "need p, q >= 1 and p + q <= %d", kMaxFeatures);
+  if (!(ridge >= 0.0) || !std::isfinite(ridge)) return fail(HF_ERR_SHAPE, "ridge must be finite and >= 0");
+  if (!mu || !cov || !A || !b) return fail(HF_ERR_NULL, "mu / cov / A / b is NULL");
+  if (!aligned_to(mu, 8) || !aligned_to(cov, 8) || !aligned_to(A, 8) || !aligned_to(b, 8) ||
+      (info && !aligned_to(info, 8)))
+    return fail(HF_ERR_SHAPE, "mu / cov / A / b / info not 8-byte aligned");
+  const size_t pq = (size_t)p + q, nA = (size_t)p * q * 8, nb = (size_t)q * 8;
+  if (overlap(A, nA, b, nb) || overlap(A, nA, mu, pq * 8) || overlap(A, nA, cov, pq * pq * 8) ||
+      overlap(b, nb, mu, pq * 8) || overlap(b, nb, cov, pq * pq * 8))
+    return fail(HF_ERR_SHAPE, "outputs A / b overlap each other or the inputs");
+  int32_t st;
+  if ((st = check_workspace(workspace, workspace_bytes, hf::recolor_solve_workspace_bytes(p, q))))
+    return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    TimedLaunch t(HF_KERNEL_RECOLOR_SOLVE, s);
+    e = hf::launch_recolor_solve(p, q, mu, cov, ridge, A, b, info, workspace, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "recolor launch");
+  return ok();
+}
+
+int32_t hf_fold_map(int32_t p, int32_t q, int32_t rank, const double* A, const double* b,
+                    const double* B, const double* G, double* A_out, double* b_out,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+  if (p < 1 || q < 1 || rank < 1 || p > kMaxFeatures || q > kMaxFeatures || rank > kMaxFeatures)
+    return fail(HF_ERR_SHAPE, "need 1 <= p, q, rank <= %d", kMaxFeatures);
+  if (!A || !b || !B || !G || !A_out || !b_out) return fail(HF_ERR_NULL, "an argument is NULL");
+  const void* ptrs[6] = {A, b, B, G, A_out, b_out};
+  for (const void* ptr : ptrs)
+    if (!aligned_to(ptr, 8)) return fail(HF_ERR_SHAPE, "pointers must be 8-byte aligned");
+  const size_t nA = (size_t)p * q * 8, nb = (size_t)q * 8, nB = (size_t)q * rank * 8;
+  if ((A_out != A && overlap(A_out, nA, A, nA)) || (b_out != b && overlap(b_out, nb, b, nb)))
+    return fail(HF_ERR_SHAPE, "A_out / b_out must be A / b exactly or not overlap them");
+  if (overlap(A_out, nA, b_out, nb) || overlap(A_out, nA, B, nB) || overlap(A_out, nA, G, nB) ||
+      overlap(b_out, nb, B, nB) || overlap(b_out, nb, G, nB) || overlap(A_out, nA, b, nb) ||
+      overlap(b_out, nb, A, nA))
+    return fail(HF_ERR_SHAPE, "outputs overlap other arguments");
+  int32_t st;
+  if ((st = check_workspace(workspace, workspace_bytes, hf::fold_workspace_bytes(p, rank)))) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    TimedLaunch t(HF_KERNEL_FOLD, s);
+    e = hf::launch_fold(p, q, rank, A, b, B, G, A_out, b_out, workspace, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "fold launch");
+  return ok();
+}
+
+int32_t hf_gemm_f64(int32_t m, int32_t n, int64_t k, const double* A, int64_t lda,
+                    int32_t a_kmajor, const double* B, int64_t ldb, int32_t b_kmajor, double* D,
+                    int64_t ldd, double alpha, double beta, const double* C, int64_t ldc,
+                    double gamma, void* stream) {
+  if (m < 1 || n < 1 || k < 0 || m > kMaxGemmRows)
+    return fail(HF_ERR_SHAPE, "need 1 <= m <= %lld, n >= 1, k >= 0", (long long)kMaxGemmRows);
+  if (!D || (k > 0 && (!A || !B))) return fail(HF_ERR_NULL, "A / B / D is NULL");
+  if (beta != 0.0 && !C) return fail(HF_ERR_NULL, "C is NULL with beta != 0");
+  if (k > 0 && (lda < (a_kmajor ? m : k) || ldb < (b_kmajor ? n : k)))
+    return fail(HF_ERR_SHAPE, "lda / ldb too small for the layouts");
+  if (ldd < n || (beta != 0.0 && ldc < n)) return fail(HF_ERR_SHAPE, "ldd / ldc < n");
+  if (!aligned_to(D, 8) || (A && !aligned_to(A, 8)) || (B && !aligned_to(B, 8)) ||
+      (C && !aligned_to(C, 8)))
+    return fail(HF_ERR_SHAPE, "pointers must be 8-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const hipError_t e = hf::launch_gemm_f64(m, n, k, A, lda, a_kmajor, B, ldb, b_kmajor, D, ldd,
+                                           alpha, beta, C, ldc, gamma, s);
+  if (e != hipSuccess) return hip_fail(e, "gemm launch");
+  return ok();
+}
+
 int32_t hf_profiler_enable(int32_t on) {
   Profiler& p = prof();
   std::lock_guard<std::mutex> g(p.mu);

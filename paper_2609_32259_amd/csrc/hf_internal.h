@@ -88,4 +88,28 @@ hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* 
                             hipStream_t s);
 hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s);
 
+// Offline map construction (fp64).  Workspace layouts are private to recolor.hip.
+int moments_chunks(long long n);
+size_t recolor_moments_workspace_bytes(long long n, int p, int q);
+// Weight sum, r, means of [x/r | y] and the centring shifts (kept in the workspace).
+hipError_t launch_recolor_stats(int dtype, long long n, int p, int q, const void* X,
+                                long long ldx, const void* Y, long long ldy, const float* w,
+                                double* r, double* mu, void* workspace, hipStream_t s);
+// Joint covariance of [x/r | y] from the shifts launch_recolor_stats left in the workspace.
+hipError_t launch_recolor_cov(int dtype, long long n, int p, int q, const void* X, long long ldx,
+                              const void* Y, long long ldy, const float* w, double* cov,
+                              void* workspace, hipStream_t s);
+size_t recolor_solve_workspace_bytes(int p, int q);
+hipError_t launch_recolor_solve(int p, int q, const double* mu, const double* cov, double lam,
+                                double* A, double* b, hf_recolor_info* info, void* workspace,
+                                hipStream_t s);
+size_t fold_workspace_bytes(int p, int rank);
+hipError_t launch_fold(int p, int q, int rank, const double* A, const double* b, const double* B,
+                       const double* G, double* A_out, double* b_out, void* workspace,
+                       hipStream_t s);
+hipError_t launch_gemm_f64(int m, int n, long long k, const double* A, long long lda, int ak,
+                           const double* B, long long ldb, int bk, double* D, long long ldd,
+                           double alpha, double beta, const double* C, long long ldc,
+                           double gamma, hipStream_t s);
+
 }  // namespace hf

@@ -30,6 +30,7 @@ HF_ALIGN_OVERLAP, HF_ALIGN_TA = 0, 1
 HF_LAYERS_INTERP2 = 0
 HF_F32, HF_BF16 = 0, 1
 HF_KERNEL_TRANSFER, HF_KERNEL_ROPE_TABLES, HF_KERNEL_ALIGNMENT, HF_KERNEL_PACK = 0, 1, 2, 3
+HF_KERNEL_MOMENTS_STATS, HF_KERNEL_MOMENTS_COV, HF_KERNEL_RECOLOR_SOLVE, HF_KERNEL_FOLD = 4, 5, 6, 7
 HF_MAX_BATCH = 64
 ALIGN_MODES = {"overlap": HF_ALIGN_OVERLAP, "ta": HF_ALIGN_TA}
 
@@ -55,6 +56,11 @@ class hf_rope(C.Structure):
 
 class hf_transfer_opts(C.Structure):
     _fields_ = [("inv_r", C.c_void_p), ("k_norm", C.c_void_p), ("k_norm_eps", C.c_float)]
+
+
+class hf_recolor_info(C.Structure):
+    _fields_ = [("iterations", C.c_int32 * 3), ("converged", C.c_int32 * 3),
+                ("residual", C.c_double * 3)]
 
 
 _I32P = C.POINTER(C.c_int32)
@@ -87,6 +93,23 @@ _SIGNATURES = {
                                         C.c_void_p, C.POINTER(hf_rope),
                                         C.POINTER(hf_transfer_opts), C.c_void_p, C.c_size_t,
                                         C.c_void_p]),
+    "hf_recolor_moments_workspace_bytes": (C.c_size_t, [C.c_int64, C.c_int32, C.c_int32]),
+    "hf_recolor_moments": (C.c_int32, [C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
+                                       C.c_int64, C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p,
+                                       C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                       C.c_void_p]),
+    "hf_recolor_solve_workspace_bytes": (C.c_size_t, [C.c_int32, C.c_int32]),
+    "hf_recolor_solve": (C.c_int32, [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p, C.c_double,
+                                     C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_size_t,
+                                     C.c_void_p]),
+    "hf_fold_workspace_bytes": (C.c_size_t, [C.c_int32, C.c_int32]),
+    "hf_fold_map": (C.c_int32, [C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                                C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                C.c_size_t, C.c_void_p]),
+    "hf_gemm_f64": (C.c_int32, [C.c_int32, C.c_int32, C.c_int64, C.c_void_p, C.c_int64,
+                                C.c_int32, C.c_void_p, C.c_int64, C.c_int32, C.c_void_p,
+                                C.c_int64, C.c_double, C.c_double, C.c_void_p, C.c_int64,
+                                C.c_double, C.c_void_p]),
     "hf_profiler_enable": (C.c_int32, [C.c_int32]),
     "hf_profiler_reset": (C.c_int32, []),
     "hf_profiler_query": (C.c_int32, [C.c_int32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
@@ -420,3 +443,152 @@ def hf_profiler_samples(kernel_id: int) -> np.ndarray:
     _check(lib().hf_profiler_samples(int(kernel_id), out.ctypes.data_as(C.POINTER(C.c_float)),
                                      out.size, C.byref(n)), "hf_profiler_samples")
     return out[:n.value]
+
+
+# ---------------------------------------------------------------------------
+# Offline construction of the maps (fp64)
+# ---------------------------------------------------------------------------
+
+def _dev_f64(t, name, numel=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or t.dtype != torch.float64 or not t.is_cuda \
+            or not t.is_contiguous():
+        raise TypeError(f"{name} must be a contiguous float64 CUDA tensor")
+    if numel is not None and t.numel() != numel:
+        raise TypeError(f"{name} must have {numel} elements")
+    return C.c_void_p(t.data_ptr())
+
+
+def _rows(t, name, width):
+    """(pointer, leading dimension) of a [n, >=width] row-major CUDA tensor."""
+    if t.dim() != 2 or t.stride(1) != 1 or t.shape[1] < width or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA tensor [n, {width}] with contiguous rows")
+    return C.c_void_p(t.data_ptr()), int(t.stride(0))
+
+
+def _workspace(ws, nbytes, dev):
+    torch = _torch()
+    if ws is None:
+        return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=dev)
+    return ws
+
+
+def hf_recolor_moments_workspace_bytes(n: int, p: int, q: int) -> int:
+    return int(lib().hf_recolor_moments_workspace_bytes(int(n), int(p), int(q)))
+
+
+def hf_recolor_moments(x, y, w=None, workspace=None, stream=None):
+    """x: [n, p], y: [n, q] CUDA tensors (fp32 or bf16, same dtype, contiguous
+    rows); w: fp32 [n] or None.  Returns (r [1], mu [p+q], cov [p+q, p+q]) as
+    float64 CUDA tensors (asynchronous)."""
+    torch = _torch()
+    if x.dtype != y.dtype or x.shape[0] != y.shape[0]:
+        raise TypeError("x and y must have the same dtype and number of rows")
+    n, p = int(x.shape[0]), int(x.shape[1])
+    q = int(y.shape[1])
+    xp, ldx = _rows(x, "x", p)
+    yp, ldy = _rows(y, "y", q)
+    wp = None
+    if w is not None:
+        if w.dtype != torch.float32 or not w.is_cuda or not w.is_contiguous() or w.numel() != n:
+            raise TypeError("w must be a contiguous float32 CUDA tensor [n]")
+        wp = C.c_void_p(w.data_ptr())
+    dev = x.device
+    r = torch.empty(1, dtype=torch.float64, device=dev)
+    mu = torch.empty(p + q, dtype=torch.float64, device=dev)
+    cov = torch.empty((p + q, p + q), dtype=torch.float64, device=dev)
+    ws = _workspace(workspace, hf_recolor_moments_workspace_bytes(n, p, q), dev)
+    st = lib().hf_recolor_moments(n, p, q, _dtype_code(x), xp, ldx, yp, ldy, wp,
+                                  C.c_void_p(r.data_ptr()), C.c_void_p(mu.data_ptr()),
+                                  C.c_void_p(cov.data_ptr()), C.c_void_p(ws.data_ptr()),
+                                  int(ws.numel() * ws.element_size()), _stream(stream))
+    _check(st, "hf_recolor_moments")
+    return r, mu, cov
+
+
+def hf_recolor_solve_workspace_bytes(p: int, q: int) -> int:
+    return int(lib().hf_recolor_solve_workspace_bytes(int(p), int(q)))
+
+
+def hf_recolor_solve(mu, cov, p: int, ridge: float = 0.0, workspace=None, stream=None):
+    """Recolor map from moments.  Returns (A [q, p], b [q], info) where A and b
+    are float64 CUDA tensors and info a CUDA byte tensor holding an
+    ``hf_recolor_info`` (read it with ``recolor_info`` after the stream is
+    done)."""
+    torch = _torch()
+    pq = int(mu.numel())
+    p = int(p)
+    q = pq - p
+    if q < 1 or p < 1:
+        raise ValueError("need 1 <= p < mu.numel()")
+    dev = mu.device
+    A = torch.empty((q, p), dtype=torch.float64, device=dev)
+    b = torch.empty(q, dtype=torch.float64, device=dev)
+    info = torch.zeros(C.sizeof(hf_recolor_info), dtype=torch.uint8, device=dev)
+    ws = _workspace(workspace, hf_recolor_solve_workspace_bytes(p, q), dev)
+    st = lib().hf_recolor_solve(p, q, _dev_f64(mu, "mu", pq), _dev_f64(cov, "cov", pq * pq),
+                                float(ridge), C.c_void_p(A.data_ptr()), C.c_void_p(b.data_ptr()),
+                                C.c_void_p(info.data_ptr()), C.c_void_p(ws.data_ptr()),
+                                int(ws.numel() * ws.element_size()), _stream(stream))
+    _check(st, "hf_recolor_solve")
+    return A, b, info
+
+
+def recolor_info(info) -> dict:
+    """Host copy of an hf_recolor_info written by hf_recolor_solve (synchronizes)."""
+    raw = bytes(info.cpu().numpy().tobytes())
+    s = hf_recolor_info.from_buffer_copy(raw)
+    return {"iterations": list(s.iterations), "converged": list(s.converged),
+            "residual": list(s.residual)}
+
+
+def hf_fold_workspace_bytes(p: int, rank: int) -> int:
+    return int(lib().hf_fold_workspace_bytes(int(p), int(rank)))
+
+
+def hf_fold_map(A, b, B, G, out=None, workspace=None, stream=None):
+    """Fold y + (y B) G into the stored map: A [q, p], b [q], B [q, rank],
+    G [rank, q] float64 CUDA tensors.  Returns (A_out, b_out) (``out`` may be
+    ``(A, b)`` for in place)."""
+    torch = _torch()
+    q, p = int(A.shape[0]), int(A.shape[1])
+    rank = int(B.shape[1]) if B.dim() == 2 else -1
+    if B.dim() != 2 or B.shape[0] != q or G.dim() != 2 or tuple(G.shape) != (rank, q):
+        raise TypeError("need B [q, rank] and G [rank, q]")
+    if out is None:
+        out = (torch.empty_like(A), torch.empty_like(b))
+    ws = _workspace(workspace, hf_fold_workspace_bytes(p, rank), A.device)
+    st = lib().hf_fold_map(p, q, rank, _dev_f64(A, "A", p * q), _dev_f64(b, "b", q),
+                           _dev_f64(B, "B", q * rank), _dev_f64(G, "G", rank * q),
+                           _dev_f64(out[0], "A_out", p * q), _dev_f64(out[1], "b_out", q),
+                           C.c_void_p(ws.data_ptr()), int(ws.numel() * ws.element_size()),
+                           _stream(stream))
+    _check(st, "hf_fold_map")
+    return out
+
+
+def hf_gemm_f64(A, B, a_kmajor=False, b_kmajor=True, alpha=1.0, beta=0.0, C_in=None, gamma=0.0,
+                out=None, stream=None):
+    """D = alpha op(A) op(B) + beta C + gamma I on float64 CUDA tensors.
+    a_kmajor: A is stored [k, m] (else [m, k]); b_kmajor: B is stored [k, n]
+    (else [n, k])."""
+    torch = _torch()
+    if A.dim() != 2 or B.dim() != 2:
+        raise TypeError("A and B must be 2-D")
+    m, k = (A.shape[1], A.shape[0]) if a_kmajor else (A.shape[0], A.shape[1])
+    kb, n = (B.shape[0], B.shape[1]) if b_kmajor else (B.shape[1], B.shape[0])
+    if kb != k:
+        raise TypeError("inner dimensions differ")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float64, device=A.device)
+    cp, ldc = (None, 0)
+    if beta != 0.0:
+        if C_in is None or tuple(C_in.shape) != (m, n):
+            raise TypeError("C_in [m, n] needed when beta != 0")
+        cp, ldc = _dev_f64(C_in, "C"), n
+    st = lib().hf_gemm_f64(int(m), int(n), int(k), _dev_f64(A, "A"), int(A.shape[1]),
+                           int(bool(a_kmajor)), _dev_f64(B, "B"), int(B.shape[1]),
+                           int(bool(b_kmajor)), _dev_f64(out, "D", m * n), int(n), float(alpha),
+                           float(beta), cp, int(ldc), float(gamma), _stream(stream))
+    _check(st, "hf_gemm_f64")
+    return out

@@ -331,3 +331,68 @@ def make_workload(cfg: Config, seed: int = 0, device="cpu", T_s: Optional[int] =
     S = make_cache(cfg, seg, seed, device)
     A, bias = make_maps(cfg, seed, device)
     return Workload(cfg, seg, S, A, bias, rope_params(cfg), make_opts(cfg, seed, device))
+
+
+# ----------------------------------------------------------------------------
+# Calibration samples for the offline map construction
+# ----------------------------------------------------------------------------
+
+@dataclass(frozen=True)
+class CalibConfig:
+    """Paired calibration features for one receiver layer and role.
+
+    n aligned tokens split over two corpora (``corpus_split`` of them in the
+    first), sender features of size p (the concatenated taps), receiver
+    features of size q."""
+    name: str
+    n: int
+    p: int
+    q: int
+    dtype: str = "f32"
+    corpus_split: float = 0.6
+    noise: float = 0.5
+    dup_block: int = 0      # >0: columns [dup_block, 2 dup_block) repeat [0, dup_block)
+
+
+CALIB_SMALL = CalibConfig("calibration 3000 tokens 100->37", n=3000, p=100, q=37)
+CALIB_14B = CalibConfig("calibration llama8b->14b-shape 2^20 tokens 3x1024->1024", n=1 << 20,
+                        p=3072, q=1024)
+CALIB_CONFIGS = {"calib-small": CALIB_SMALL, "calib-14b": CALIB_14B}
+
+
+def make_calibration(cfg: CalibConfig, seed: int = 0, device="cpu"):
+    """Seeded samples (x [n, p], y [n, q], w [n]).
+
+    x: independent N(0, (1 + k)^-1) channels k = 0..p-1 (a decaying spectrum),
+    mixed by two random Householder reflections, times per-channel log-normal
+    scales (sigma 0.5), plus per-channel offsets N(0, 0.25).  y: x times a
+    N(0, 1/p) matrix, plus N(0, noise^2) noise and offsets N(0, 0.25).  Weights
+    give the two corpora equal total weight (1/2 each, uniform inside a
+    corpus).  x and y are stored in cfg.dtype; w is fp32."""
+    torch = _torch()
+    seqs = np.random.SeedSequence(seed).spawn(3)
+    g = _torch_gen(seqs[0], device)
+    f32 = torch.float32
+    n, p, q = cfg.n, cfg.p, cfg.q
+    var = 1.0 / torch.sqrt(1.0 + torch.arange(p, dtype=f32, device=device))
+    x = torch.randn((n, p), generator=g, dtype=f32, device=device) * var
+    for _ in range(2):
+        v = torch.randn(p, generator=g, dtype=f32, device=device)
+        v = v / torch.linalg.vector_norm(v)
+        x -= 2.0 * (x @ v)[:, None] * v[None, :]
+    x *= torch.exp(0.5 * torch.randn(p, generator=g, dtype=f32, device=device))
+    x += 0.5 * torch.randn(p, generator=g, dtype=f32, device=device)
+    if cfg.dup_block:
+        x[:, cfg.dup_block:2 * cfg.dup_block] = x[:, :cfg.dup_block]
+    g2 = _torch_gen(seqs[1], device)
+    Cm = torch.randn((p, q), generator=g2, dtype=f32, device=device) / float(np.sqrt(p))
+    y = x @ Cm
+    y += cfg.noise * torch.randn((n, q), generator=g2, dtype=f32, device=device)
+    y += 0.5 * torch.randn(q, generator=g2, dtype=f32, device=device)
+    n_a = max(1, min(n - 1, int(round(cfg.corpus_split * n)))) if n > 1 else n
+    w = torch.empty(n, dtype=f32, device=device)
+    w[:n_a] = 0.5 / n_a
+    if n > n_a:
+        w[n_a:] = 0.5 / (n - n_a)
+    dt = f32 if cfg.dtype == "f32" else torch.bfloat16
+    return x.to(dt), y.to(dt), w

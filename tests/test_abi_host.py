@@ -214,3 +214,68 @@ def test_transfer_taps_host_validation(L):
     bad[1, 0] = -1
     assert call(tp=bad) == -2
     assert call(sd=_desc(d=64), rd=_desc(L_=6, d=64)) == -8    # bf16 needs d_h = 128
+
+
+def test_recolor_host_validation(L):
+    fake = C.c_void_p(0x10000)
+    ws = C.c_void_p(0x100000)
+    big = 1 << 40
+    # moments: n, sizes, dtype, NULLs, leading dimensions, workspace
+    args = lambda **k: dict(dict(n=100, p=8, q=4, dtype=0, x=fake, ldx=8, y=fake, ldy=4, w=None,
+                                 r=C.c_void_p(0x20000), mu=C.c_void_p(0x30000),
+                                 cov=C.c_void_p(0x40000), ws=ws, wsb=big), **k)
+    def mom(a):
+        return L.hf_recolor_moments(a["n"], a["p"], a["q"], a["dtype"], a["x"], a["ldx"], a["y"],
+                                    a["ldy"], a["w"], a["r"], a["mu"], a["cov"], a["ws"],
+                                    a["wsb"], None)
+    assert mom(args(n=0)) == -2
+    assert mom(args(p=0)) == -2
+    assert mom(args(p=40000, q=40000)) == -2
+    assert mom(args(dtype=7)) == -5
+    assert mom(args(x=None)) == -1
+    assert mom(args(ldx=7)) == -2
+    assert mom(args(mu=C.c_void_p(0x40000 + 8))) == -2      # inside cov
+    assert mom(args(ws=None)) == -1
+    assert mom(args(ws=C.c_void_p(0x100000 + 16))) == -2    # not 256-B aligned
+    assert mom(args(wsb=16)) == -6
+    assert hf.hf_recolor_moments_workspace_bytes(1 << 20, 3072, 1024) > 0
+    assert L.hf_recolor_moments_workspace_bytes(0, 3, 3) == 0
+    # solve
+    def sol(p=8, q=4, mu=C.c_void_p(0x30000), cov=C.c_void_p(0x40000), ridge=0.0,
+            A=C.c_void_p(0x80000), b=C.c_void_p(0x90000), ws=ws, wsb=big):
+        return L.hf_recolor_solve(p, q, mu, cov, ridge, A, b, None, ws, wsb, None)
+    assert sol(p=0) == -2
+    assert sol(ridge=-1.0) == -2
+    assert sol(ridge=float("nan")) == -2
+    assert sol(ridge=float("inf")) == -2
+    assert sol(A=None) == -1
+    assert sol(A=C.c_void_p(0x40000)) == -2                 # output over the input
+    assert sol(b=C.c_void_p(0x80000 + 8)) == -2             # b inside A
+    assert sol(wsb=8) == -6
+    assert sol(A=C.c_void_p(0x80004)) == -2                 # misaligned
+    assert hf.hf_recolor_solve_workspace_bytes(3072, 1024) > 5 * 3072 * 3072 * 8
+    # fold
+    def fold(p=8, q=4, rank=2, A=C.c_void_p(0x80000), b=C.c_void_p(0x90000),
+             B=C.c_void_p(0xA0000), G=C.c_void_p(0xB0000), Ao=C.c_void_p(0xC0000),
+             bo=C.c_void_p(0xD0000), wsb=big):
+        return L.hf_fold_map(p, q, rank, A, b, B, G, Ao, bo, ws, wsb, None)
+    assert fold(rank=0) == -2
+    assert fold(G=None) == -1
+    assert fold(Ao=C.c_void_p(0x80000 + 8)) == -2          # partial overlap with A
+    assert fold(Ao=C.c_void_p(0xA0000)) == -2              # over B
+    assert fold(wsb=0) == -6
+    assert hf.hf_fold_workspace_bytes(3072, 16) >= 16 * 3072 * 8
+    # product
+    def gemm(m=4, n=4, k=4, A=fake, lda=4, ak=0, B=fake, ldb=4, bk=1, D=C.c_void_p(0x50000),
+             ldd=4, beta=0.0, Cp=None, ldc=0):
+        return L.hf_gemm_f64(m, n, k, A, lda, ak, B, ldb, bk, D, ldd, 1.0, beta, Cp, ldc, 0.0,
+                             None)
+    assert gemm(m=0) == -2
+    assert gemm(m=65535 * 64 + 1) == -2
+    assert gemm(k=-1) == -2
+    assert gemm(D=None) == -1
+    assert gemm(beta=1.0) == -1
+    assert gemm(lda=3) == -2
+    assert gemm(ak=1, lda=3) == -2
+    assert gemm(ldd=3) == -2
+    assert gemm(beta=1.0, Cp=fake, ldc=3) == -2

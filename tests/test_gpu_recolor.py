@@ -1,0 +1,280 @@
+"""GPU parity of the offline map construction (fp64) against the oracle.
+
+Tolerances.  Every result is fp64 on both sides; they differ only in the
+order of the sums and, for the solve, in the method (Newton-Schulz iterations
+on the GPU, eigendecomposition and SVD in the oracle).
+  * products: |D - ref| <= 4 k eps (|alpha| |op(A)| |op(B)|) + 4 eps |ref|,
+    the standard bound for a length-k dot product in any summation order;
+  * moments: the same bound over the n samples of the centred products;
+  * solve: 1e-8 relative (Frobenius).  The roots are accurate to about
+    kappa(S) eps ~ 1e-12 for these inputs (kappa <= 1e4), and each iteration
+    stops at a residual near rounding.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import recolor as rc
+
+pytestmark = pytest.mark.gpu
+
+EPS = np.finfo(np.float64).eps
+
+
+@pytest.fixture(scope="module")
+def hf():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_32259_amd import heterofold
+    heterofold.lib()
+    return heterofold
+
+
+def _dev(a):
+    import torch
+    return torch.as_tensor(np.ascontiguousarray(a, np.float64), device="cuda")
+
+
+def _np(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def _bound(absA, absB, k, ref, alpha=1.0):
+    return 4 * max(k, 1) * EPS * abs(alpha) * (absA @ absB) + 4 * EPS * np.abs(ref) + 1e-300
+
+
+@pytest.mark.parametrize("ak,bk", [(False, True), (True, True), (False, False), (True, False)])
+@pytest.mark.parametrize("m,n,k", [(70, 45, 37), (128, 64, 200), (1, 1, 1), (65, 129, 16),
+                                   (200, 3, 513)])
+def test_gemm_layouts(hf, ak, bk, m, n, k):
+    rng = np.random.default_rng(m * 1000 + n * 10 + k)
+    opA = rng.standard_normal((m, k))
+    opB = rng.standard_normal((k, n))
+    Cin = rng.standard_normal((m, n))
+    A = opA.T.copy() if ak else opA
+    B = opB if bk else opB.T.copy()
+    alpha, beta, gamma = -0.75, 0.5, 1.25
+    D = hf.hf_gemm_f64(_dev(A), _dev(B), a_kmajor=ak, b_kmajor=bk, alpha=alpha, beta=beta,
+                       C_in=_dev(Cin), gamma=gamma)
+    ref = alpha * (opA @ opB) + beta * Cin + gamma * np.eye(m, n)
+    got = _np(D)
+    assert np.all(np.abs(got - ref) <= _bound(np.abs(opA), np.abs(opB), k, ref, alpha)
+                  + 4 * EPS * (abs(beta) * np.abs(Cin) + abs(gamma)))
+
+
+def test_gemm_in_place_and_empty_k(hf):
+    import torch
+    rng = np.random.default_rng(3)
+    A = rng.standard_normal((33, 20))
+    B = rng.standard_normal((20, 33))
+    Cin = rng.standard_normal((33, 33))
+    D = _dev(Cin)
+    hf.hf_gemm_f64(_dev(A), _dev(B), alpha=2.0, beta=-1.0, C_in=D, out=D)
+    ref = 2.0 * A @ B - Cin
+    assert np.abs(_np(D) - ref).max() <= 1e-12 * np.abs(ref).max()
+    # k = 0: D = beta C + gamma I exactly
+    E = hf.hf_gemm_f64(torch.zeros((33, 0), dtype=torch.float64, device="cuda"),
+                       torch.zeros((0, 33), dtype=torch.float64, device="cuda"), beta=3.0,
+                       C_in=_dev(Cin), gamma=0.5)
+    np.testing.assert_array_equal(_np(E), 3.0 * Cin + 0.5 * np.eye(33))
+
+
+def _moments_check(hf, x, y, w):
+    import torch
+    r, mu, cov = hf.hf_recolor_moments(x, y, w)
+    X = x.double().cpu().numpy()
+    Y = y.double().cpu().numpy()
+    W = None if w is None else w.double().cpu().numpy()
+    r_ref = rc.sender_rms(X, W)
+    mz, my, Szz, Szy, Syy = rc.weighted_moments(X / r_ref, Y, W)
+    p = X.shape[1]
+    got_r, got_mu, got_cov = _np(r)[0], _np(mu), _np(cov)
+    n = X.shape[0]
+    assert abs(got_r - r_ref) <= 8 * n * EPS * r_ref
+    mu_ref = np.concatenate([mz, my])
+    V = np.hstack([X / r_ref, Y])
+    absmean = (np.abs(V).T @ (np.ones(n) if W is None else W)) / (n if W is None else W.sum())
+    assert np.all(np.abs(got_mu - mu_ref) <= 8 * n * EPS * absmean + 1e-300)
+    J = np.block([[Szz, Szy], [Szy.T, Syy]])
+    Vc = np.abs(V - mu_ref)
+    Wv = np.ones(n) if W is None else W
+    scale = (Vc * Wv[:, None]).T @ Vc / Wv.sum()
+    # an error d in a mean moves the centred products by d |v - mu| (first order
+    # cancels in the weighted sum; kept here as a safe margin) and d_i d_j
+    E = 8 * n * EPS * absmean
+    m = (Vc * Wv[:, None]).sum(0) / Wv.sum()
+    extra = 2 * (np.outer(E, m) + np.outer(m, E)) + np.outer(E, E)
+    assert np.all(np.abs(got_cov - J) <= 16 * n * EPS * scale + extra + 1e-300)
+    np.testing.assert_array_equal(got_cov, got_cov.T)
+    return got_r, got_mu, got_cov
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("weighted", [True, False])
+def test_moments_match_oracle(hf, dtype, weighted):
+    import dataclasses
+    from paper_2609_32259_amd import synth
+    cfg = dataclasses.replace(synth.CALIB_SMALL, dtype=dtype)
+    x, y, w = synth.make_calibration(cfg, seed=1, device="cuda")
+    _moments_check(hf, x, y, w if weighted else None)
+
+
+@pytest.mark.parametrize("n,p,q", [(1, 3, 2), (2, 1, 1), (257, 64, 64), (700, 5, 130)])
+def test_moments_edge_sizes(hf, n, p, q):
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(n + p + q)
+    x = torch.randn((n, p), generator=g, device="cuda") + 3.0
+    y = torch.randn((n, q), generator=g, device="cuda")
+    w = torch.rand(n, generator=g, device="cuda") + 0.1
+    _moments_check(hf, x, y, w)
+
+
+def test_moments_strided_rows(hf):
+    import torch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    big = torch.randn((400, 90), generator=g, device="cuda")
+    x, y = big[:, :50], big[:, 60:85]   # row strides 90, not contiguous tensors
+    _moments_check(hf, x, y, None)
+
+
+def _solve_ref(mu, cov, p, lam):
+    A, b = rc.recolor(mu[:p], mu[p:], cov[:p, :p], cov[:p, p:], cov[p:, p:], lam)
+    return rc.abi_orientation(A), b
+
+
+def _rel(a, b):
+    return np.linalg.norm(a - b) / np.linalg.norm(b)
+
+
+@pytest.mark.parametrize("p,q,lam", [(100, 37, 0.0), (100, 37, 1e-3), (37, 100, 0.0),
+                                     (64, 64, 0.0), (1, 1, 0.0), (130, 1, 0.0)])
+def test_solve_matches_oracle(hf, p, q, lam):
+    from paper_2609_32259_amd import synth
+    cfg = synth.CalibConfig("solve", n=4000, p=p, q=q)
+    x, y, w = synth.make_calibration(cfg, seed=2, device="cuda")
+    r, mu, cov = hf.hf_recolor_moments(x, y, w)
+    A, b, info = hf.hf_recolor_solve(mu, cov, p, ridge=lam)
+    inf = hf.recolor_info(info)
+    assert inf["converged"] == [1, 1, 1], inf
+    A_ref, b_ref = _solve_ref(_np(mu), _np(cov), p, lam)
+    assert _rel(_np(A), A_ref) <= 1e-8
+    assert _rel(_np(b), b_ref) <= 1e-8 or np.abs(_np(b) - b_ref).max() <= 1e-8 * np.abs(A_ref).max()
+
+
+def test_solve_identities_and_duplicated_taps(hf):
+    # A clipped tap repeats a sender layer: S_Z is singular and needs the ridge.
+    from paper_2609_32259_amd import synth
+    cfg = synth.CalibConfig("dup", n=5000, p=120, q=40, dup_block=30)
+    x, y, w = synth.make_calibration(cfg, seed=3, device="cuda")
+    r, mu, cov = hf.hf_recolor_moments(x, y, w)
+    lam = 1e-4
+    A, b, info = hf.hf_recolor_solve(mu, cov, 120, ridge=lam)
+    assert hf.recolor_info(info)["converged"] == [1, 1, 1]
+    M, c, Am, bm = _np(mu), _np(cov), _np(A), _np(b)
+    A_ref, b_ref = _solve_ref(M, c, 120, lam)
+    assert _rel(Am, A_ref) <= 1e-7
+    # the paper's identities for the stabilized covariances
+    Sz = rc.ridge(c[:120, :120], lam)
+    Sy = rc.ridge(c[120:, 120:], lam)
+    np.testing.assert_allclose(Am @ Sz @ Am.T, Sy, rtol=1e-8, atol=1e-10 * np.abs(Sy).max())
+    np.testing.assert_allclose(Am @ M[:120] + bm, M[120:], rtol=1e-10, atol=1e-12)
+
+
+def test_solve_reports_an_indefinite_covariance(hf):
+    import torch
+    p, q = 4, 2
+    cov = np.eye(p + q)
+    cov[1, 1] = -1.0   # not a covariance: the root iteration cannot converge
+    mu = np.zeros(p + q)
+    A, b, info = hf.hf_recolor_solve(_dev(mu), _dev(cov), p)
+    torch.cuda.synchronize()
+    assert hf.recolor_info(info)["converged"][0] == 0
+
+
+@pytest.mark.parametrize("p,q,rank", [(100, 37, 16), (64, 64, 1), (3, 70, 5)])
+def test_fold_matches_oracle(hf, p, q, rank):
+    rng = np.random.default_rng(p + q + rank)
+    A = rng.standard_normal((q, p))   # stored orientation
+    b = rng.standard_normal(q)
+    B = 0.02 * rng.standard_normal((q, rank))
+    G = rng.standard_normal((rank, q))
+    Af_ref, bf_ref = rc.fold(A.T, b, B, G)
+    Af, bf = hf.hf_fold_map(_dev(A), _dev(b), _dev(B), _dev(G))
+    assert _rel(_np(Af), Af_ref.T) <= 1e-14 * max(q, rank)
+    assert _rel(_np(bf), bf_ref) <= 1e-14 * max(q, rank)
+    # in place
+    Ad, bd = _dev(A), _dev(b)
+    hf.hf_fold_map(Ad, bd, _dev(B), _dev(G), out=(Ad, bd))
+    np.testing.assert_array_equal(_np(Ad), _np(Af))
+    np.testing.assert_array_equal(_np(bd), _np(bf))
+
+
+def test_recolored_map_drives_the_transfer(hf):
+    """Samples -> moments -> Recolor -> fold on the GPU, then the folded map in
+    hf_transfer_kv_taps, against the oracle doing the same steps from the same
+    samples and transferring with the map it built."""
+    import torch
+    from oracle import alignment as al
+    from oracle import layer_map as lm
+    from oracle import transfer as tr
+    from paper_2609_32259_amd import synth
+    from paper_2609_32259_amd.path import TransferPath
+    from _parity import check_layer
+
+    cfg = synth.TINY_F32.with_(name="tiny-f32 neighbor3 recolored", layer_map="neighbor3",
+                               L_s=6, L_r=4)
+    wl = synth.make_workload(cfg, seed=4, device="cuda")
+    p, q = cfg.d_map_in, cfg.d_r
+    x, y, w = synth.make_calibration(synth.CalibConfig("tiny", n=2000, p=p, q=q), seed=4,
+                                     device="cuda")
+    rng = np.random.default_rng(9)
+    B = 0.02 * rng.standard_normal((q, 4))
+    G = 0.1 * rng.standard_normal((4, q))
+    print(f"[gpu-recolor] end to end p={p} q={q} n=2000", flush=True)
+    r, mu, cov = hf.hf_recolor_moments(x, y, w)
+    A, b, info = hf.hf_recolor_solve(mu, cov, p, ridge=1e-6)
+    Af, bf = hf.hf_fold_map(A, b, _dev(B), _dev(G))
+    assert hf.recolor_info(info)["converged"] == [1, 1, 1]
+    # oracle: the same construction from the same samples
+    X, Y, W = (t.double().cpu().numpy() for t in (x, y, w))
+    r_ref, A_ref, b_ref = rc.recolor_from_samples(X, Y, W, lam=1e-6)
+    Af_ref, bf_ref = rc.fold(A_ref, b_ref, B, G)
+    assert abs(float(_np(r)[0]) - r_ref) <= 1e-12 * r_ref
+    assert _rel(_np(Af), rc.abi_orientation(Af_ref)) <= 1e-8
+    assert _rel(_np(bf), bf_ref) <= 1e-8
+    # the map the transfer takes: 1/r through the options, A and b in fp32
+    inv_r = torch.full((cfg.L_r, 2), 1.0 / float(_np(r)[0]), dtype=torch.float32, device="cuda")
+    wl.A = Af.to(torch.float32).expand(cfg.L_r, 2, q, p).contiguous()
+    wl.bias = bf.to(torch.float32).expand(cfg.L_r, 2, q).contiguous()
+    opts = dict(inv_r=inv_r, k_norm=None, k_norm_eps=1e-6)
+    path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r,
+                        layer_map="neighbor3", opts=opts)
+    path.step()
+    torch.cuda.synchronize()
+    taps = lm.neighbor3(cfg.L_s, cfg.L_r)
+    A_o = np.broadcast_to(rc.abi_orientation(Af_ref), (cfg.L_r, 2, q, p))
+    b_o = np.broadcast_to(bf_ref, (cfg.L_r, 2, q))
+    ropts = {"inv_r": np.full((cfg.L_r, 2), 1.0 / r_ref)}
+    for bi in range(wl.seg.batch):
+        T_r = int(wl.seg.r_len[bi])
+        if T_r == 0:
+            continue
+        sb, se, rb, re_ = wl.seg.seq(bi)
+        csr = al.build_alignment(sb, se, rb, re_, "overlap")
+        T_s = int(wl.seg.s_len[bi])
+        S = wl.S[bi, :, :, :, :T_s, :].double().cpu().numpy()
+        rp = None
+        if wl.rope is not None:
+            rp = dict(wl.rope)
+            for k in ("pos0_s", "pos0_r"):
+                rp[k] = 0 if wl.rope.get(k) is None else int(np.asarray(wl.rope[k])[bi])
+        ref = tr.transfer_taps(S, taps, csr, A_o, b_o, rp, H_r=cfg.H_r, opts=ropts)
+        got = path.R[bi, :, :, :, :T_r, :].double().cpu().numpy()
+        for l in range(cfg.L_r):
+            for c in range(2):
+                check_layer(got[l, c], ref[l, c], f"recolored b={bi} l={l} c={c}", dtype="f32")
