@@ -420,8 +420,9 @@ typedef enum {
   HF_KERNEL_ROPE_TABLES = 1,/* cos/sin table kernel of hf_transfer_kv */
   HF_KERNEL_ALIGNMENT = 2,  /* the three kernels of hf_build_alignment, together */
   HF_KERNEL_PACK = 3,       /* hf_pack_maps */
-  HF_KERNEL_MOMENTS_STATS = 4, /* the column-statistics kernels of hf_recolor_moments */
-  HF_KERNEL_MOMENTS_COV = 5,   /* the covariance product of hf_recolor_moments */
+  HF_KERNEL_MOMENTS_STATS = 4, /* hf_recolor_moments: column statistics, then the sum of
+                                  the covariance partials (two timed groups per call) */
+  HF_KERNEL_MOMENTS_COV = 5,   /* hf_recolor_moments: the covariance product kernel */
   HF_KERNEL_RECOLOR_SOLVE = 6, /* all launches of hf_recolor_solve */
   HF_KERNEL_FOLD = 7,          /* all launches of hf_fold_map */
   HF_KERNEL_COUNT = 8

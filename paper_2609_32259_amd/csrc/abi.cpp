@@ -659,9 +659,14 @@ int32_t hf_recolor_moments(int64_t n, int32_t p, int32_t q, int32_t dtype, const
   if (e != hipSuccess) return hip_fail(e, "moments statistics launch");
   {
     TimedLaunch t(HF_KERNEL_MOMENTS_COV, s);
-    e = hf::launch_recolor_cov(dtype, n, p, q, x, ldx, y, ldy, w, cov, workspace, s);
+    e = hf::launch_recolor_cov(dtype, n, p, q, x, ldx, y, ldy, w, workspace, s);
   }
   if (e != hipSuccess) return hip_fail(e, "covariance launch");
+  {
+    TimedLaunch t(HF_KERNEL_MOMENTS_STATS, s);
+    e = hf::launch_recolor_cov_reduce(n, p, q, cov, workspace, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "covariance reduction launch");
   return ok();
 }
 

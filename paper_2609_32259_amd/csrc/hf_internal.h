@@ -95,10 +95,13 @@ size_t recolor_moments_workspace_bytes(long long n, int p, int q);
 hipError_t launch_recolor_stats(int dtype, long long n, int p, int q, const void* X,
                                 long long ldx, const void* Y, long long ldy, const float* w,
                                 double* r, double* mu, void* workspace, hipStream_t s);
-// Joint covariance of [x/r | y] from the shifts launch_recolor_stats left in the workspace.
+// Partial Gram tiles of the centred samples, from the shifts launch_recolor_stats
+// left in the workspace; then their fixed-order sum into the joint covariance.
 hipError_t launch_recolor_cov(int dtype, long long n, int p, int q, const void* X, long long ldx,
-                              const void* Y, long long ldy, const float* w, double* cov,
-                              void* workspace, hipStream_t s);
+                              const void* Y, long long ldy, const float* w, void* workspace,
+                              hipStream_t s);
+hipError_t launch_recolor_cov_reduce(long long n, int p, int q, double* cov, void* workspace,
+                                     hipStream_t s);
 size_t recolor_solve_workspace_bytes(int p, int q);
 hipError_t launch_recolor_solve(int p, int q, const double* mu, const double* cov, double lam,
                                 double* A, double* b, hf_recolor_info* info, void* workspace,

@@ -39,8 +39,6 @@ struct NsState {
   double res;  // last residual |I - P|_F
 };
 
-enum GemmMode { kPlain = 0, kJoint = 1 };
-
 struct GemmArgs {
   int m, n;
   long long k;
@@ -55,51 +53,13 @@ struct GemmArgs {
   double alpha, beta, gamma;  // D = alpha * op(A) op(B) + beta * C + gamma * I
   const double* alpha_dev;    // multiplies alpha, or nullptr
   const int* skip;            // nothing is done while *skip != 0, or nullptr
-  int sym;                    // upper tiles only, each written to D[i][j] and D[j][i]
-  // kJoint: op(A) = op(B)^T = V^T diag(w) and op(B) = V, V = [X | Y] (k rows),
-  // each column c centred by shift[c] and scaled by scale[c].
-  const void* X;
-  long long ldx;
-  const void* Y;
-  long long ldy;
-  int p;
-  const double* shift;
-  const double* scale;
-  const float* w;
 };
-
-__device__ inline double load_elem(const float* p, long long i) { return (double)p[i]; }
-__device__ inline double load_elem(const uint16_t* p, long long i) {
-  return (double)__uint_as_float(((uint32_t)p[i]) << 16);
-}
-
-// Element (row kk, column c) of V = [X | Y] for the joint moments, centred and scaled.
-template <typename T>
-__device__ inline double joint_elem(const GemmArgs& g, long long kk, int c) {
-  const double v = c < g.p ? load_elem(static_cast<const T*>(g.X), kk * g.ldx + c)
-                           : load_elem(static_cast<const T*>(g.Y), kk * g.ldy + (c - g.p));
-  return (v - g.shift[c]) * g.scale[c];
-}
 
 // Stage one kBK x kBM slice of op(A) (As[kk][i]) and op(B) (Bs[kk][j]) in
 // registers: each of the 256 threads holds 4 elements of each.
-template <int MODE, typename T, bool AK, bool BK>
+template <bool AK, bool BK>
 __device__ inline void gemm_load(const GemmArgs& g, int m0, int n0, long long k0, int tid,
                                  double (&ra)[4], double (&rb)[4]) {
-  if (MODE == kJoint) {
-    // both operands are V read row by row: thread = (kk, 4 consecutive columns)
-    const int kk = tid >> 4, c4 = (tid & 15) * 4;
-    const long long row = k0 + kk;
-    const bool rok = row < g.k;
-    const double wk = (rok && g.w) ? (double)g.w[row] : 1.0;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int ci = m0 + c4 + e, cj = n0 + c4 + e;
-      ra[e] = (rok && ci < g.m) ? joint_elem<T>(g, row, ci) * wk : 0.0;
-      rb[e] = (rok && cj < g.n) ? joint_elem<T>(g, row, cj) : 0.0;
-    }
-    return;
-  }
   if (AK) {  // op(A)(i, kk) = A[kk * lda + i]
     const int kk = tid >> 4, i4 = (tid & 15) * 4;
     const long long row = k0 + kk;
@@ -134,10 +94,10 @@ __device__ inline void gemm_load(const GemmArgs& g, int m0, int n0, long long k0
   }
 }
 
-template <int MODE, bool AK, bool BK>
+template <bool AK, bool BK>
 __device__ inline void gemm_store(double (*As)[kBM + kPad], double (*Bs)[kBN + kPad], int tid,
                                   const double (&ra)[4], const double (&rb)[4]) {
-  if (MODE == kJoint || AK) {
+  if (AK) {
     const int kk = tid >> 4, i4 = (tid & 15) * 4;
 #pragma unroll
     for (int e = 0; e < 4; ++e) As[kk][i4 + e] = ra[e];
@@ -146,7 +106,7 @@ __device__ inline void gemm_store(double (*As)[kBM + kPad], double (*Bs)[kBN + k
 #pragma unroll
     for (int e = 0; e < 4; ++e) As[k4 + e][i] = ra[e];
   }
-  if (MODE == kJoint || BK) {
+  if (BK) {
     const int kk = tid >> 4, j4 = (tid & 15) * 4;
 #pragma unroll
     for (int e = 0; e < 4; ++e) Bs[kk][j4 + e] = rb[e];
@@ -161,11 +121,10 @@ __device__ inline void gemm_store(double (*As)[kBM + kPad], double (*Bs)[kBN + k
 // 32 x 32 block as 2 x 2 matrix-core tiles of 16 x 16.  The fp64 MFMA reads
 // op(A)(i, k) from lane i + 16 k and op(B)(k, j) from lane j + 16 k, and leaves
 // D(lane / 16 + 4 v, lane % 16) in element v of each lane (rows interleaved).
-template <int MODE, typename T, bool AK, bool BK>
+template <bool AK, bool BK>
 __global__ __launch_bounds__(kGemmThreads) void gemm_f64_kernel(GemmArgs g) {
   if (g.skip && *g.skip) return;
   const int tm = blockIdx.y, tn = blockIdx.x;
-  if (g.sym && tm > tn) return;
   __shared__ double As[2][kBK][kBM + kPad];
   __shared__ double Bs[2][kBK][kBN + kPad];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -181,15 +140,15 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_f64_kernel(GemmArgs g) {
 
   double ra[4], rb[4];
   if (nk > 0) {
-    gemm_load<MODE, T, AK, BK>(g, m0, n0, 0, tid, ra, rb);
-    gemm_store<MODE, AK, BK>(As[0], Bs[0], tid, ra, rb);
+    gemm_load<AK, BK>(g, m0, n0, 0, tid, ra, rb);
+    gemm_store<AK, BK>(As[0], Bs[0], tid, ra, rb);
   }
   __syncthreads();
   const int li = lane & 15, lk = lane >> 4;
   for (long long kt = 0; kt < nk; ++kt) {
     const int cur = (int)(kt & 1);
     const bool more = kt + 1 < nk;
-    if (more) gemm_load<MODE, T, AK, BK>(g, m0, n0, (kt + 1) * kBK, tid, ra, rb);
+    if (more) gemm_load<AK, BK>(g, m0, n0, (kt + 1) * kBK, tid, ra, rb);
 #pragma unroll
     for (int ks = 0; ks < kBK / 4; ++ks) {
       double a[2], b[2];
@@ -204,12 +163,11 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_f64_kernel(GemmArgs g) {
         for (int y = 0; y < 2; ++y)
           acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x], b[y], acc[x][y], 0, 0, 0);
     }
-    if (more) gemm_store<MODE, AK, BK>(As[cur ^ 1], Bs[cur ^ 1], tid, ra, rb);
+    if (more) gemm_store<AK, BK>(As[cur ^ 1], Bs[cur ^ 1], tid, ra, rb);
     __syncthreads();
   }
 
   const double alpha = g.alpha_dev ? g.alpha * *g.alpha_dev : g.alpha;
-  const bool diag_tile = tm == tn;
 #pragma unroll
   for (int x = 0; x < 2; ++x)
 #pragma unroll
@@ -219,13 +177,202 @@ __global__ __launch_bounds__(kGemmThreads) void gemm_f64_kernel(GemmArgs g) {
         const int i = m0 + wm * 32 + x * 16 + lk + 4 * v;
         const int j = n0 + wn * 32 + y * 16 + li;
         if (i >= g.m || j >= g.n) continue;
-        if (g.sym && diag_tile && i > j) continue;  // the mirror of (j, i) writes it
         double val = alpha * acc[x][y][v];
         if (g.beta != 0.0) val += g.beta * g.C[(long long)i * g.ldc + j];
         if (i == j) val += g.gamma;
         g.D[(long long)i * g.ldd + j] = val;
-        if (g.sym && i != j) g.D[(long long)j * g.ldd + i] = val;
       }
+}
+
+// ---------------------------------------------------------------------------
+// Weighted, centred Gram product of the samples V = [X | Y] (n rows, m = p + q
+// columns): G = (V - 1 shift^T)^T diag(w) (V - 1 shift^T), upper 128 x 128
+// tiles only, the rows split into `splits` ranges whose partial tiles a second
+// kernel adds up in a fixed order.  Work item = (split, tile), split-major, so
+// the workgroups resident together stream the same rows.
+// ---------------------------------------------------------------------------
+constexpr int kCT = 128;   // tile edge
+constexpr int kCK = 16;    // rows per step
+constexpr int kCPad = 4;
+constexpr int kCovResident = 512;  // workgroups resident at once (2 per CU)
+
+struct CovArgs {
+  long long n;
+  int p, m;
+  const void* X;
+  long long ldx;
+  const void* Y;
+  long long ldy;
+  const float* w;
+  const double* shift;  // [m]
+  int nt;               // tiles per edge
+  int n_tiles;          // nt (nt + 1) / 2
+  long long rows_per_split;
+  int vec;              // column groups of 8 are 16-byte aligned and never straddle X | Y
+  double* partial;      // [splits][n_tiles][kCT][kCT]
+};
+
+__device__ inline void load8(const float* p, float (&v)[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+__device__ inline void load8(const uint16_t* p, float (&v)[8]) {
+  const uint4 a = *reinterpret_cast<const uint4*>(p);
+  const uint32_t u[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[2 * e] = __uint_as_float(u[e] << 16);
+    v[2 * e + 1] = __uint_as_float(u[e] & 0xffff0000u);
+  }
+}
+__device__ inline float load1(const float* p) { return *p; }
+__device__ inline double load_elem(const float* p, long long i) { return (double)p[i]; }
+__device__ inline double load_elem(const uint16_t* p, long long i) {
+  return (double)__uint_as_float(((uint32_t)p[i]) << 16);
+}
+__device__ inline float load1(const uint16_t* p) { return __uint_as_float(((uint32_t)*p) << 16); }
+
+// Eight consecutive columns c0..c0+7 of sample row r (zeros past m).
+template <typename T>
+__device__ inline void cov_load(const CovArgs& g, long long r, int c0, float (&v)[8]) {
+  const T* X = static_cast<const T*>(g.X);
+  const T* Y = static_cast<const T*>(g.Y);
+  if (g.vec) {
+    if (c0 >= g.m) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = 0.f;
+    } else if (c0 < g.p) {
+      load8(X + r * g.ldx + c0, v);
+    } else {
+      load8(Y + r * g.ldy + (c0 - g.p), v);
+    }
+    return;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int c = c0 + e;
+    v[e] = c >= g.m ? 0.f : (c < g.p ? load1(X + r * g.ldx + c) : load1(Y + r * g.ldy + (c - g.p)));
+  }
+}
+
+// 256 threads = 4 waves in a 2 x 2 grid, each owning 64 x 64 as 4 x 4 MFMA tiles.
+template <typename T>
+__global__ __launch_bounds__(256) void cov_kernel(CovArgs g) {
+  __shared__ double As[2][kCK][kCT + kCPad];
+  __shared__ double Bs[2][kCK][kCT + kCPad];
+  const int item = blockIdx.x;
+  const int split = item / g.n_tiles, tile = item - split * g.n_tiles;
+  int tm = 0, rem = tile;
+  while (rem >= g.nt - tm) {
+    rem -= g.nt - tm;
+    ++tm;
+  }
+  const int tn = tm + rem;
+  const long long r_beg = (long long)split * g.rows_per_split;
+  const long long r_end = r_beg + g.rows_per_split < g.n ? r_beg + g.rows_per_split : g.n;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int li = lane & 15, lk = lane >> 4;
+
+  // staging role: one row (kk) and eight consecutive columns (c8) of each operand
+  const int kk = tid >> 4, c8 = (tid & 15) * 8;
+  const int ca = tm * kCT + c8, cb = tn * kCT + c8;
+  double sha[8], shb[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    sha[e] = ca + e < g.m ? g.shift[ca + e] : 0.0;
+    shb[e] = cb + e < g.m ? g.shift[cb + e] : 0.0;
+  }
+
+  double4_t acc[4][4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) acc[x][y] = double4_t{0.0, 0.0, 0.0, 0.0};
+
+  float va[8], vb[8];
+  float wr = 0.f;
+  auto fetch = [&](long long k0) {
+    const long long r = k0 + kk;
+    if (r < r_end) {
+      cov_load<T>(g, r, ca, va);
+      cov_load<T>(g, r, cb, vb);
+      wr = g.w ? g.w[r] : 1.f;
+    } else {
+      wr = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) va[e] = vb[e] = 0.f;
+    }
+  };
+  auto stage = [&](int buf) {
+    const double wd = (double)wr;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      // rows past the range carry weight 0 on the A side and stage 0 on the B side
+      As[buf][kk][c8 + e] = ((double)va[e] - sha[e]) * wd;
+      Bs[buf][kk][c8 + e] = wr != 0.f ? (double)vb[e] - shb[e] : 0.0;
+    }
+  };
+
+  const long long nk = (r_end - r_beg + kCK - 1) / kCK;
+  if (nk > 0) {
+    fetch(r_beg);
+    stage(0);
+  }
+  __syncthreads();
+  for (long long kt = 0; kt < nk; ++kt) {
+    const int cur = (int)(kt & 1);
+    const bool more = kt + 1 < nk;
+    if (more) fetch(r_beg + (kt + 1) * kCK);
+#pragma unroll
+    for (int ks = 0; ks < kCK / 4; ++ks) {
+      double a[4], b[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        a[x] = As[cur][ks * 4 + lk][wm * 64 + x * 16 + li];
+        b[x] = Bs[cur][ks * 4 + lk][wn * 64 + x * 16 + li];
+      }
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[x], b[y], acc[x][y], 0, 0, 0);
+    }
+    if (more) stage(cur ^ 1);
+    __syncthreads();
+  }
+
+  double* out = g.partial + ((long long)split * g.n_tiles + tile) * (kCT * kCT);
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        out[(wm * 64 + x * 16 + lk + 4 * v) * kCT + wn * 64 + y * 16 + li] = acc[x][y][v];
+}
+
+// cov[i][j] = scale_i scale_j / W * sum over splits of the (min, max) entry:
+// both triangles from the upper tiles, so the result is exactly symmetric.
+__global__ __launch_bounds__(256) void cov_reduce_kernel(const double* partial, int splits,
+                                                          int n_tiles, int nt, int m,
+                                                          const double* scale,
+                                                          const double* inv_w, double* cov) {
+  const long long total = (long long)m * m;
+  const double iw = *inv_w;
+  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (long long)gridDim.x * blockDim.x) {
+    const int i = (int)(e / m), j = (int)(e - (long long)i * m);
+    const int a = i < j ? i : j, b = i < j ? j : i;
+    const int tm = a / kCT, tn = b / kCT;
+    const long long tile = (long long)tm * nt - (long long)tm * (tm - 1) / 2 + (tn - tm);
+    const long long off = tile * (kCT * kCT) + (a - tm * kCT) * kCT + (b - tn * kCT);
+    double s = 0.0;
+    for (int k = 0; k < splits; ++k) s += partial[(long long)k * n_tiles * (kCT * kCT) + off];
+    cov[e] = s * scale[i] * scale[j] * iw;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -444,10 +591,10 @@ int grid_for(long long total, int threads = 256, int cap = 4096) {
   return (int)(b < cap ? b : cap);
 }
 
-template <int MODE, typename T, bool AK, bool BK>
+template <bool AK, bool BK>
 hipError_t gemm_launch(const GemmArgs& g, hipStream_t s) {
   dim3 grid((g.n + kBN - 1) / kBN, (g.m + kBM - 1) / kBM);
-  hipLaunchKernelGGL((gemm_f64_kernel<MODE, T, AK, BK>), grid, dim3(kGemmThreads), 0, s, g);
+  hipLaunchKernelGGL((gemm_f64_kernel<AK, BK>), grid, dim3(kGemmThreads), 0, s, g);
   return hipGetLastError();
 }
 
@@ -476,10 +623,10 @@ hipError_t gemm(int m, int n, long long k, const double* A, long long lda, bool 
   g.gamma = gamma;
   g.alpha_dev = alpha_dev;
   g.skip = skip;
-  if (ak && bk) return gemm_launch<kPlain, float, true, true>(g, s);
-  if (ak) return gemm_launch<kPlain, float, true, false>(g, s);
-  if (bk) return gemm_launch<kPlain, float, false, true>(g, s);
-  return gemm_launch<kPlain, float, false, false>(g, s);
+  if (ak && bk) return gemm_launch<true, true>(g, s);
+  if (ak) return gemm_launch<true, false>(g, s);
+  if (bk) return gemm_launch<false, true>(g, s);
+  return gemm_launch<false, false>(g, s);
 }
 
 #define HF_CHECK(x)                   \
@@ -620,12 +767,52 @@ int moments_chunks(long long n) {
   return (int)c;
 }
 
+namespace {
+
+struct CovPlan {
+  int nt, n_tiles, splits;
+  long long rows_per_split;
+};
+
+// Rows are split so that the (split, tile) items fill the resident workgroups
+// with the least idle tail, each split keeping at least 32 steps of rows.
+CovPlan cov_plan(long long n, int m) {
+  CovPlan c;
+  c.nt = (m + kCT - 1) / kCT;
+  c.n_tiles = c.nt * (c.nt + 1) / 2;
+  const long long steps = (n + kCK - 1) / kCK;
+  long long max_splits = steps / 32;
+  if (max_splits < 1) max_splits = 1;
+  if (max_splits > 64) max_splits = 64;
+  int best = 1;
+  double best_waste = 1e30;
+  for (int s = 1; s <= max_splits; ++s) {
+    const long long items = (long long)s * c.n_tiles;
+    if (items < kCovResident && s < max_splits) continue;
+    const long long rounds = (items + kCovResident - 1) / kCovResident;
+    const double waste = (double)(rounds * kCovResident) / (double)items - 1.0;
+    if (waste < best_waste - 0.01) {
+      best_waste = waste;
+      best = s;
+    }
+  }
+  c.splits = best;
+  c.rows_per_split = (steps + best - 1) / best * kCK;
+  return c;
+}
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+}  // namespace
+
 size_t recolor_moments_workspace_bytes(long long n, int p, int q) {
   const size_t n_chunks = (size_t)moments_chunks(n);
   const size_t pq = (size_t)p + q;
-  auto a = [](size_t b) { return (b + 255) / 256 * 256; };
-  return a(n_chunks * pq * 8) + a(n_chunks * (size_t)p * 8) + a(n_chunks * 8) + a(pq * 8) +
-         a((size_t)p * 8) + 2 * a(pq * 8) + a(8);
+  const CovPlan c = cov_plan(n, p + q);
+  return align256(n_chunks * pq * 8) + align256(n_chunks * (size_t)p * 8) +
+         align256(n_chunks * 8) + align256(pq * 8) + align256((size_t)p * 8) +
+         2 * align256(pq * 8) + align256(8) +
+         align256((size_t)c.splits * c.n_tiles * kCT * kCT * 8);
 }
 
 hipError_t launch_recolor_stats(int dtype, long long n, int p, int q, const void* X,
@@ -665,8 +852,8 @@ hipError_t launch_recolor_stats(int dtype, long long n, int p, int q, const void
 }
 
 hipError_t launch_recolor_cov(int dtype, long long n, int p, int q, const void* X, long long ldx,
-                              const void* Y, long long ldy, const float* w, double* cov,
-                              void* workspace, hipStream_t s) {
+                              const void* Y, long long ldy, const float* w, void* workspace,
+                              hipStream_t s) {
   const int n_chunks = moments_chunks(n);
   const int pq = p + q;
   Carve cv{static_cast<char*>(workspace)};
@@ -678,25 +865,52 @@ hipError_t launch_recolor_cov(int dtype, long long n, int p, int q, const void* 
   double* shift = cv.take<double>(pq);
   double* scale = cv.take<double>(pq);
   double* inv_w = cv.take<double>(1);
-  GemmArgs g{};
+  const CovPlan plan = cov_plan(n, pq);
+  double* partial = cv.take<double>((size_t)plan.splits * plan.n_tiles * kCT * kCT);
+  CovArgs g{};
+  g.n = n;
+  g.p = p;
   g.m = pq;
-  g.n = pq;
-  g.k = n;
-  g.D = cov;
-  g.ldd = pq;
-  g.alpha = 1.0;
-  g.alpha_dev = inv_w;
-  g.sym = 1;
   g.X = X;
   g.ldx = ldx;
   g.Y = Y;
   g.ldy = ldy;
-  g.p = p;
-  g.shift = shift;
-  g.scale = scale;
   g.w = w;
-  if (dtype == HF_BF16) return gemm_launch<kJoint, uint16_t, true, true>(g, s);
-  return gemm_launch<kJoint, float, true, true>(g, s);
+  g.shift = shift;
+  g.nt = plan.nt;
+  g.n_tiles = plan.n_tiles;
+  g.rows_per_split = plan.rows_per_split;
+  g.partial = partial;
+  const int per16 = dtype == HF_BF16 ? 8 : 4;  // elements per 16 bytes
+  g.vec = (p % 8 == 0) && (q % 8 == 0) && (ldx % per16 == 0) && (ldy % per16 == 0) &&
+          ((uintptr_t)X % 16 == 0) && ((uintptr_t)Y % 16 == 0);
+  const unsigned items = (unsigned)((long long)plan.splits * plan.n_tiles);
+  if (dtype == HF_BF16)
+    hipLaunchKernelGGL(cov_kernel<uint16_t>, dim3(items), dim3(256), 0, s, g);
+  else
+    hipLaunchKernelGGL(cov_kernel<float>, dim3(items), dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_recolor_cov_reduce(long long n, int p, int q, double* cov, void* workspace,
+                                     hipStream_t s) {
+  const int n_chunks = moments_chunks(n);
+  const int pq = p + q;
+  Carve cv{static_cast<char*>(workspace)};
+  (void)cv.take<double>((size_t)n_chunks * pq);
+  (void)cv.take<double>((size_t)n_chunks * p);
+  (void)cv.take<double>(n_chunks);
+  (void)cv.take<double>(pq);
+  (void)cv.take<double>(p);
+  (void)cv.take<double>(pq);
+  double* scale = cv.take<double>(pq);
+  double* inv_w = cv.take<double>(1);
+  const CovPlan plan = cov_plan(n, pq);
+  double* partial = cv.take<double>((size_t)plan.splits * plan.n_tiles * kCT * kCT);
+  hipLaunchKernelGGL(cov_reduce_kernel, dim3(grid_for((long long)pq * pq, 256, 8192)), dim3(256),
+                     0, s, (const double*)partial, plan.splits, plan.n_tiles, plan.nt, pq,
+                     (const double*)scale, (const double*)inv_w, cov);
+  return hipGetLastError();
 }
 
 size_t recolor_solve_workspace_bytes(int p, int q) {

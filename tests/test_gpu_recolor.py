@@ -122,15 +122,68 @@ def test_moments_match_oracle(hf, dtype, weighted):
     _moments_check(hf, x, y, w if weighted else None)
 
 
-@pytest.mark.parametrize("n,p,q", [(1, 3, 2), (2, 1, 1), (257, 64, 64), (700, 5, 130)])
-def test_moments_edge_sizes(hf, n, p, q):
+@pytest.mark.parametrize("n,p,q,dtype", [(1, 3, 2, "f32"), (2, 1, 1, "f32"), (257, 64, 64, "f32"),
+                                         (700, 5, 130, "f32"), (5000, 200, 136, "f32"),
+                                         (5000, 200, 136, "bf16"), (1100, 8, 256, "bf16")])
+def test_moments_edge_sizes(hf, n, p, q, dtype):
+    # p, q multiples of 8 take the 16-byte load path; several tiles and splits
     import torch
     g = torch.Generator(device="cuda")
     g.manual_seed(n + p + q)
-    x = torch.randn((n, p), generator=g, device="cuda") + 3.0
-    y = torch.randn((n, q), generator=g, device="cuda")
+    dt = torch.float32 if dtype == "f32" else torch.bfloat16
+    x = (torch.randn((n, p), generator=g, device="cuda") + 3.0).to(dt)
+    y = torch.randn((n, q), generator=g, device="cuda").to(dt)
     w = torch.rand(n, generator=g, device="cuda") + 0.1
     _moments_check(hf, x, y, w)
+
+
+def test_moments_full_width_sampled(hf):
+    """3x1024 -> 1024 features (the 14B-shape map), 2^16 samples: r and the
+    means in full, the covariance on sampled entries, exact symmetry."""
+    import torch
+    from paper_2609_32259_amd import synth
+    cfg = synth.CalibConfig("full width", n=1 << 16, p=3072, q=1024)
+    print(f"[gpu-recolor] moments n={cfg.n} p={cfg.p} q={cfg.q}", flush=True)
+    x, y, w = synth.make_calibration(cfg, seed=7, device="cuda")
+    r, mu, cov = hf.hf_recolor_moments(x, y, w)
+    got_r, got_mu, got_cov = _np(r)[0], _np(mu), _np(cov)
+    np.testing.assert_array_equal(got_cov, got_cov.T)
+    X = x.double().cpu().numpy()
+    Y = y.double().cpu().numpy()
+    W = w.double().cpu().numpy()
+    n = cfg.n
+    r_ref = rc.sender_rms(X, W)
+    assert abs(got_r - r_ref) <= 8 * n * EPS * r_ref
+    mu_ref = np.concatenate([(W @ X) / W.sum() / r_ref, (W @ Y) / W.sum()])
+    np.testing.assert_allclose(got_mu, mu_ref, rtol=1e-11, atol=1e-12)
+    rng = np.random.default_rng(0)
+    V = lambda c: X[:, c] / r_ref if c < cfg.p else Y[:, c - cfg.p]   # noqa: E731
+    for i, j in rng.integers(0, cfg.p + cfg.q, size=(64, 2)):
+        ci = V(i) - mu_ref[i]
+        cj = V(j) - mu_ref[j]
+        ref = float(np.sum(W * ci * cj) / W.sum())
+        tol = 16 * n * EPS * float(np.sum(W * np.abs(ci) * np.abs(cj)) / W.sum()) + 1e-15
+        assert abs(got_cov[i, j] - ref) <= tol, (i, j, got_cov[i, j], ref)
+
+
+def test_solve_full_width_identities(hf):
+    """The full-size solve (3072 x 1024) checked by the paper's identities for
+    the stabilized covariances: A S_Z A^T = S_Y and A mu_Z + b = mu_Y."""
+    from paper_2609_32259_amd import synth
+    cfg = synth.CalibConfig("full width", n=1 << 15, p=3072, q=1024)
+    x, y, w = synth.make_calibration(cfg, seed=8, device="cuda")
+    lam = 1e-6
+    print(f"[gpu-recolor] solve p={cfg.p} q={cfg.q} ridge={lam}", flush=True)
+    r, mu, cov = hf.hf_recolor_moments(x, y, w)
+    A, b, info = hf.hf_recolor_solve(mu, cov, cfg.p, ridge=lam)
+    inf = hf.recolor_info(info)
+    print(f"[gpu-recolor] {inf}", flush=True)
+    assert inf["converged"] == [1, 1, 1]
+    M, c, Am, bm = _np(mu), _np(cov), _np(A), _np(b)
+    Sz = rc.ridge(c[:cfg.p, :cfg.p], lam)
+    Sy = rc.ridge(c[cfg.p:, cfg.p:], lam)
+    assert _rel(Am @ Sz @ Am.T, Sy) <= 1e-8
+    np.testing.assert_allclose(Am @ M[:cfg.p] + bm, M[cfg.p:], rtol=1e-9, atol=1e-10)
 
 
 def test_moments_strided_rows(hf):
