@@ -863,8 +863,8 @@ hipError_t launch_recolor_cov(int dtype, long long n, int p, int q, const void* 
   (void)cv.take<double>(pq);
   (void)cv.take<double>(p);
   double* shift = cv.take<double>(pq);
-  double* scale = cv.take<double>(pq);
-  double* inv_w = cv.take<double>(1);
+  (void)cv.take<double>(pq);  // column scales (applied by the reduction)
+  (void)cv.take<double>(1);   // 1 / W
   const CovPlan plan = cov_plan(n, pq);
   double* partial = cv.take<double>((size_t)plan.splits * plan.n_tiles * kCT * kCT);
   CovArgs g{};
