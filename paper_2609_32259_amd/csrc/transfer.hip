@@ -309,10 +309,9 @@ __device__ __forceinline__ void epilogue_rows(const TransferArgs& p, f32x16* acc
 //          in fp32 -- gather the tile's CSR entries (staged in LDS), mix the
 //          two sender-layer taps, un-rotate keys, weight and sum -- and store
 //          it once as bf16 in LDS.  Sender rows come straight from global
-//          memory through a two-stage register pipeline; no matrix-core work is
-//          in flight, so nothing waits behind these loads.  Rows are handed to
-//          waves sorted by entry count, so the 8 rows of a wave take the same
-//          number of loop trips.
+//          memory through a register ring of trips; no matrix-core work is in
+//          flight, so nothing waits behind these loads.  Each lane group walks
+//          a run of rows holding an equal share of the tile's entries.
 //   mma:   each wave multiplies its output tiles by X over all d_in/16 k-steps
 //          (v_mfma_f32_32x32x16_bf16: packed map fragment from global memory as
 //          A, X from LDS as B) with a four-deep register prefetch of the map
@@ -342,7 +341,8 @@ constexpr int kXBytes = 64 * kXF * 2;
 constexpr int kDtBytes = kDMax * kDH * 4;            // U(delta) rows: cos | sin, fp32
 constexpr int kOffDt = kXBytes;
 constexpr int kOffEnt = kOffDt + kDtBytes;
-constexpr int kEntInts = 65 + 64 + kEMax * 3 + 4;    // estart, gbase, ecol, ew, einfo, misc
+// estart, gbase, ecol, ew, einfo, misc, gstart, row min / max sender index
+constexpr int kEntInts = 65 + 64 + kEMax * 3 + 4 + 65 + 2 * 64;
 constexpr int kSmemBytes = kOffEnt + kEntInts * 4;
 // Store phase, inside the (then free) X region: receiver RoPE rows, bias, staging.
 constexpr int kOffRcs = 0;                           // [64][cos 64 | sin 64] fp32
@@ -352,11 +352,12 @@ constexpr int kOffRsum = kOffStage + 8 * 32 * kXS * 2;  // 8 waves x 32 fp32
 static_assert(kOffRsum + 8 * 32 * 4 <= kXBytes, "store phase must fit the X region");
 static_assert(kSmemBytes <= 160 * 1024, "LDS budget");
 
-// Group-walk build.  Wave w builds sender head w / WPH for 8 RPG consecutive
-// tile rows (WPH = 8 / RPG waves share a head); lane group g (8 lanes, 16
-// features each) walks the CSR entries of RPG consecutive rows in order, one
-// entry per trip, so a sender token shared by neighbouring rows is read twice
-// in a row (the second read hits the cache).  Trips past a group's last entry
+// Group-walk build.  WPH waves share a sender head, 8 WPH lane groups (8
+// lanes, 16 features each) over the tile's 64 rows: group g walks the CSR
+// entries of a run of consecutive rows in order, one entry per trip, so a
+// sender token shared by neighbouring rows is read twice in a row (the second
+// read hits the cache).  The runs hold equal shares of the tile's entries, as
+// a wave takes as many trips as its longest run.  Trips past a group's last entry
 // use an out-of-range buffer offset, which returns zeros without touching
 // memory, so every trip issues the same loads and a ring of R trips keeps
 // R - 1 trips of loads in flight.
@@ -524,6 +525,9 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   float* ew = reinterpret_cast<float*>(ecol + kEMax);
   int* einfo = reinterpret_cast<int*>(ew + kEMax);
   int* flag = einfo + kEMax;  // [0]: the staged build does not apply
+  int* gstart = flag + 4;     // lane group g walks tile rows [gstart[g], gstart[g + 1])
+  int* rmin = gstart + 65;    // smallest / largest sender index of each tile row
+  int* rmax = rmin + 64;
 
   const Item it = decode_item(p, blockIdx.x);
   const Ctx cx = make_ctx(p, it);
@@ -534,9 +538,8 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   const int g0 = p.row0[it.b] + j0;
   const bool unrot = cx.cs_s != nullptr;
   const int H = p.H_s;
-  // WPH waves share a sender head; a lane group walks RPG consecutive rows
+  // WPH waves share a sender head; each lane group walks a run of rows
   const int WPH = H == 1 ? 8 : H == 2 ? 4 : H <= 4 ? 2 : 1;
-  const int RPG = 8 / WPH;
 
   // ---- stage the tile's alignment entries ----
   if (tid <= 64) estart[tid] = p.row_ptr[g0 + min(tid, nrows)];
@@ -564,19 +567,40 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
     }
   }
   __syncthreads();
-  if (wave == 0) {  // lane = tile row: sender span of each lane group's rows
-    int lmin = INT_MAX, lmax = -1;
+  const int NG = 8 * WPH;  // lane groups over the tile's rows
+  if (wave == 0) {
+    // Contiguous runs of rows with equal shares of the tile's entries: the
+    // build of a wave takes as many trips as its longest run.
+    if (lane <= NG) {
+      int b = lane == NG ? 64 : 0;
+      if (lane > 0 && lane < NG) {
+        const int target = (lane * nnz + NG / 2) / NG;
+        int lo = 0, hi = nrows;  // smallest r with estart[r] - e_base >= target
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (estart[mid] - e_base >= target) hi = mid; else lo = mid + 1;
+        }
+        b = lo;
+      }
+      gstart[lane] = b;
+    }
+    int lmin = INT_MAX, lmax = -1;  // lane = tile row
     if (staged)
       for (int k = estart[lane] - e_base; k < estart[lane + 1] - e_base; ++k) {
         lmin = min(lmin, ecol[k]);
         lmax = max(lmax, ecol[k]);
       }
-    for (int o = 1; o < RPG; o <<= 1) {
-      lmin = min(lmin, __shfl_xor(lmin, o));
-      lmax = max(lmax, __shfl_xor(lmax, o));
+    rmin[lane] = lmin;
+    rmax[lane] = lmax;
+    if (lane < NG) {  // sender span of each run
+      int gmin = INT_MAX, gmax = -1;
+      for (int r = gstart[lane]; r < gstart[lane + 1]; ++r) {
+        gmin = min(gmin, rmin[r]);
+        gmax = max(gmax, rmax[r]);
+      }
+      gbase[lane] = gmax < 0 ? 0 : gmin;
+      if (unrot && gmax >= 0 && gmax - gmin >= kDMax) flag[0] = 1;
     }
-    gbase[lane] = lmax < 0 ? 0 : lmin;
-    if (unrot && lmax >= 0 && lmax - lmin >= kDMax) flag[0] = 1;
   }
   __builtin_amdgcn_s_waitcnt(0);  // the rotation table has landed
   __syncthreads();
@@ -609,22 +633,24 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
       const int sh = wave / WPH;  // sender head this wave builds
       if (sh < H) {
         const GroupLds L{estart, ecol, ew, einfo, dt, e_base};
-        const int r_first = (wave % WPH) * 8 * RPG + (lane >> 3) * RPG;
-        const int base = gbase[r_first];
+        const int grp = (wave % WPH) * 8 + (lane >> 3);
+        const int r_first = gstart[grp];
+        const int rpg = gstart[grp + 1] - r_first;
+        const int base = gbase[grp];
         if (MULTI) {  // one sender layer per tap
           if (tap == 0) {
-            if (unrot) build_groups<false, true, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
-            else build_groups<false, false, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+            if (unrot) build_groups<false, true, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+            else build_groups<false, false, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
           } else {
-            if (unrot) build_groups<false, true, 2>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
-            else build_groups<false, false, 2>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+            if (unrot) build_groups<false, true, 2>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+            else build_groups<false, false, 2>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
           }
         } else if (ct.two_tap) {
-          if (unrot) build_groups<true, true, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
-          else build_groups<true, false, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+          if (unrot) build_groups<true, true, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+          else build_groups<true, false, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
         } else {
-          if (unrot) build_groups<false, true, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
-          else build_groups<false, false, 4>(ct, p, L, base, sh, r_first, RPG, lane, Xs);
+          if (unrot) build_groups<false, true, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+          else build_groups<false, false, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
         }
       }
     } else {
