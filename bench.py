@@ -322,12 +322,13 @@ def main():
     k_ms, k_n = hf.hf_profiler_query(hf.HF_KERNEL_TRANSFER)
     a_ms, a_n = hf.hf_profiler_query(hf.HF_KERNEL_ALIGNMENT)
     r_ms, r_n = hf.hf_profiler_query(hf.HF_KERNEL_ROPE_TABLES)
+    g_ms, g_n = hf.hf_profiler_query(hf.HF_KERNEL_TRANSFER_STAGE)
     k_avg = k_ms / max(k_n, 1)
     ks = hf.hf_profiler_samples(hf.HF_KERNEL_TRANSFER).astype(np.float64)
     k_med, k_min, k_p90 = (float(np.median(ks)), float(ks.min()), float(np.percentile(ks, 90)))
     log(f"[bench] step {ms_step:.3f} ms; transfer kernel mean {k_avg:.3f} ms, median {k_med:.3f}, "
         f"min {k_min:.3f}, p90 {k_p90:.3f} (x{k_n}); alignment {a_ms / max(a_n, 1):.3f} ms; "
-        f"rope tables {r_ms / max(r_n, 1):.3f} ms")
+        f"rope tables {r_ms / max(r_n, 1):.3f} ms; tile staging {g_ms / max(g_n, 1):.3f} ms")
 
     flops, bytes_alg = algorithmic_cost(cfg, wl.seg)
     achieved = flops / (k_avg * 1e-3) / 1e12
@@ -338,6 +339,7 @@ def main():
             "kernel_ms_median": round(k_med, 4), "kernel_ms_min": round(k_min, 4),
             "kernel_ms_p90": round(k_p90, 4),
             "alignment_ms": round(a_ms / max(a_n, 1), 4),
+            "tile_staging_ms": round(g_ms / max(g_n, 1), 4),
             "algorithmic_bytes": bytes_alg,
             "hbm_GBps_algorithmic": round(bytes_alg / (k_avg * 1e-3) / 1e9, 1)}
     cpu = None

@@ -230,7 +230,13 @@ size_t hf_packed_maps_bytes(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtyp
 int32_t hf_pack_maps(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype, const void* A,
                      void* A_packed, void* stream);
 
-/* Workspace bytes hf_transfer_kv needs (RoPE cos/sin tables); 0 without RoPE. */
+/*
+ * Workspace bytes hf_transfer_kv and hf_transfer_kv_taps need: the RoPE
+ * cos/sin tables (none without RoPE) and, for bf16 with 4 or 8 receiver heads
+ * and at most 8 sender heads, an 8 KB staging record per 64-row receiver tile
+ * (the tile's alignment entries, written once per call and read by every
+ * receiver layer and role).  0 when neither applies.
+ */
 size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
                                    const hf_kv_desc* sender, const hf_kv_desc* receiver,
                                    const hf_rope* rope);
@@ -425,7 +431,8 @@ typedef enum {
   HF_KERNEL_MOMENTS_COV = 5,   /* hf_recolor_moments: the covariance product kernel */
   HF_KERNEL_RECOLOR_SOLVE = 6, /* all launches of hf_recolor_solve */
   HF_KERNEL_FOLD = 7,          /* all launches of hf_fold_map */
-  HF_KERNEL_COUNT = 8
+  HF_KERNEL_TRANSFER_STAGE = 8,/* per-tile alignment staging of hf_transfer_kv (bf16, tiled) */
+  HF_KERNEL_COUNT = 9
 } hf_kernel_id;
 
 /*

@@ -357,6 +357,19 @@ int32_t rope_sizes(int32_t B, const int32_t* s_len, const int32_t* r_len, const 
 
 size_t rope_bytes(int P, int d_h) { return align_up((size_t)P * d_h * sizeof(float), 256); }
 
+// Staging records of the row tiles (one per tile of the batch), where the
+// kernel that runs keeps them.
+size_t record_bytes(int32_t B, const int32_t* r_len, const hf_kv_desc* sender,
+                    const hf_kv_desc* receiver) {
+  const size_t per = hf::transfer_tile_record_bytes(sender->dtype, receiver->H, sender->H,
+                                                    sender->d_h);
+  if (per == 0) return 0;
+  const int rt = hf::transfer_rows_per_tile(sender->dtype, receiver->H, sender->H, 1, sender->d_h);
+  size_t tiles = 0;
+  for (int b = 0; b < B; ++b) tiles += r_len[b] > 0 ? ((size_t)r_len[b] + rt - 1) / rt : 0;
+  return tiles * per;
+}
+
 }  // namespace
 
 size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
@@ -365,7 +378,8 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
   if (B < 1 || B > HF_MAX_BATCH || !s_len || !r_len || !sender || !receiver) return 0;
   RopeSizes rs;
   if (rope_sizes(B, s_len, r_len, rope, rs) != HF_OK) return 0;
-  return rope_bytes(rs.P_s, sender->d_h) + rope_bytes(rs.P_r, receiver->d_h);
+  return rope_bytes(rs.P_s, sender->d_h) + rope_bytes(rs.P_r, receiver->d_h) +
+         record_bytes(B, r_len, sender, receiver);
 }
 
 namespace {
@@ -456,7 +470,8 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
   }
   RopeSizes rs;
   if ((st = rope_sizes(B, s_len, r_len, rope, rs))) return st;
-  const size_t ws_need = rope_bytes(rs.P_s, d_h) + rope_bytes(rs.P_r, d_h);
+  const size_t rec_off = rope_bytes(rs.P_s, d_h) + rope_bytes(rs.P_r, d_h);
+  const size_t ws_need = rec_off + record_bytes(B, r_len, sender, receiver);
   if (ws_need > 0) {
     if (!workspace) return fail(HF_ERR_NULL, "workspace is NULL");
     if (workspace_bytes < ws_need)
@@ -537,6 +552,7 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
     a.cs_r = reinterpret_cast<const float*>(w + rope_bytes(rs.P_s, d_h));
     a.rot = 1;
   }
+  if (ws_need > rec_off) a.tile_rec = reinterpret_cast<const int32_t*>(w + rec_off);
   if (tiles == 0) return ok();
   hipError_t e = hipSuccess;
   if (a.unrot || a.rot) {
@@ -546,6 +562,11 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
       e = hf::launch_rope_table(const_cast<float*>(a.cs_r), rs.P_r, d_h, rope->theta_r, s);
   }
   if (e != hipSuccess) return hip_fail(e, "RoPE table launch");
+  if (a.tile_rec) {
+    TimedLaunch t(HF_KERNEL_TRANSFER_STAGE, s);
+    e = hf::launch_transfer_stage(dtype, a, s);
+  }
+  if (e != hipSuccess) return hip_fail(e, "tile staging launch");
   {
     TimedLaunch t(HF_KERNEL_TRANSFER, s);
     e = hf::launch_transfer(dtype, a, s);

@@ -304,9 +304,10 @@ __device__ __forceinline__ void epilogue_rows(const TransferArgs& p, f32x16* acc
 // receiver heads, NTW = 2 for 4).
 //
 // One workgroup = 8 waves computes 64 receiver rows x all d_r receiver
-// features of one (layer, role), in three phases:
+// features of one (layer, role), in three phases after copying the tile's
+// staging record (stage_tiles_kernel) into LDS:
 //   build: all 512 threads form the whole aligned feature block X[64][d_in]
-//          in fp32 -- gather the tile's CSR entries (staged in LDS), mix the
+//          in fp32 -- gather the tile's CSR entries (from the record), mix the
 //          two sender-layer taps, un-rotate keys, weight and sum -- and store
 //          it once as bf16 in LDS.  Sender rows come straight from global
 //          memory through a register ring of trips; no matrix-core work is in
@@ -327,11 +328,11 @@ __device__ __forceinline__ void epilogue_rows(const TransferArgs& p, f32x16* acc
 // feat[q] + 8 (i/4) + 4 (l/32) + i%4.
 //
 // The un-rotation of sender row i at position p_i is split as
-// U(p_i) = U(q_r) U(p_i - q_r) with q_r the position of the first sender token
-// of receiver row r: the small-offset rotations U(0..15) sit in LDS and the
-// per-row U(q_r) is applied once to each head's sum.  Tiles whose entry count
-// or in-row sender span exceed what is staged build X entry by entry from the
-// CSR and the full RoPE table in global memory (same results).
+// U(p_i) = U(q_g) U(p_i - q_g) with q_g the position of the smallest sender
+// token of the lane group's run: the small-offset rotations U(0..15) sit in
+// LDS and U(q_g) is applied once to each row's sum.  Tiles whose entry count or
+// run sender span exceed what is staged build X entry by entry from the CSR
+// and the full RoPE table in global memory (same results).
 // ---------------------------------------------------------------------------
 constexpr int kEMax = 512;             // CSR entries staged per tile
 constexpr int kDMax = kRopeDeltaRows;  // in-row sender offsets handled with the LDS table
@@ -341,9 +342,13 @@ constexpr int kXBytes = 64 * kXF * 2;
 constexpr int kDtBytes = kDMax * kDH * 4;            // U(delta) rows: cos | sin, fp32
 constexpr int kOffDt = kXBytes;
 constexpr int kOffEnt = kOffDt + kDtBytes;
-// estart, gbase, ecol, ew, einfo, misc, gstart, row min / max sender index
+// Staged tile record: estart, gbase, ecol, ew, einfo, flags, gstart, row min /
+// max sender index; written once per row tile by the staging kernel and copied
+// whole into LDS by every (layer, role) of the tile.
 constexpr int kEntInts = 65 + 64 + kEMax * 3 + 4 + 65 + 2 * 64;
-constexpr int kSmemBytes = kOffEnt + kEntInts * 4;
+constexpr int kRecBytes = 8192;  // 8 waves x 64 lanes x 16 bytes
+static_assert(kEntInts * 4 <= kRecBytes, "tile record size");
+constexpr int kSmemBytes = kOffEnt + kRecBytes;
 // Store phase, inside the (then free) X region: receiver RoPE rows, bias, staging.
 constexpr int kOffRcs = 0;                           // [64][cos 64 | sin 64] fp32
 constexpr int kOffBias = kOffRcs + 64 * kDH * 4;     // [d_r <= 1024] fp32
@@ -367,7 +372,7 @@ struct GroupLds {
   const int* estart;  // [65] CSR offsets of the tile rows
   const int* ecol;    // staged sender indices
   const float* ew;    // staged weights num / den
-  const int* einfo;   // staged row | last-entry-of-row << 8
+  const int* einfo;   // staged row | last-entry-of-row << 8 | first-entry-of-row << 9
   const float* dt;    // U(0..15), swizzled
   int e_base;
 };
@@ -514,65 +519,63 @@ __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& 
   }
 }
 
-template <int NTW, bool MULTI>
-__global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const TransferArgs p) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[kSmemBytes];
-  uint16_t* Xs = reinterpret_cast<uint16_t*>(smem);
-  float* dt = reinterpret_cast<float*>(smem + kOffDt);
-  int* estart = reinterpret_cast<int*>(smem + kOffEnt);
+// ---------------------------------------------------------------------------
+// Per-tile staging for the tiled kernel, one workgroup per 64-row tile of the
+// batch.  The record holds the tile's CSR entries with their row, weight
+// num/den and first / last-of-row flags; the cut of the rows into runs of
+// consecutive rows with equal shares of the entries (a wave takes as many
+// trips as its longest run); each run's smallest sender index; and two flags:
+// [0] some run spans kDMax sender tokens or more (too wide for the LDS
+// rotation table), [1] the tile has more than kEMax entries.  Every (layer,
+// role) of the tile reads the same record.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(512) void stage_tiles_kernel(const TransferArgs p, int* rec) {
+  __shared__ __attribute__((aligned(16))) int ent[kRecBytes / 4];
+  int* estart = ent;
   int* gbase = estart + 65;
   int* ecol = gbase + 64;
   float* ew = reinterpret_cast<float*>(ecol + kEMax);
   int* einfo = reinterpret_cast<int*>(ew + kEMax);
-  int* flag = einfo + kEMax;  // [0]: the staged build does not apply
+  int* flag = einfo + kEMax;
   int* gstart = flag + 4;     // lane group g walks tile rows [gstart[g], gstart[g + 1])
   int* rmin = gstart + 65;    // smallest / largest sender index of each tile row
   int* rmax = rmin + 64;
 
-  const Item it = decode_item(p, blockIdx.x);
-  const Ctx cx = make_ctx(p, it);
+  const int t = blockIdx.x;
+  int b = 0;
+  while (b + 1 < p.B && p.tile_start[b + 1] <= t) ++b;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int Tr = p.Tr[it.b];
-  const int j0 = it.tile * 64;
-  const int nrows = min(64, Tr - j0);
-  const int g0 = p.row0[it.b] + j0;
-  const bool unrot = cx.cs_s != nullptr;
+  const int j0 = (t - p.tile_start[b]) * 64;
+  const int nrows = min(64, p.Tr[b] - j0);
+  const int g0 = p.row0[b] + j0;
+  const int Ts = p.Ts[b];
   const int H = p.H_s;
-  // WPH waves share a sender head; each lane group walks a run of rows
-  const int WPH = H == 1 ? 8 : H == 2 ? 4 : H <= 4 ? 2 : 1;
+  const int WPH = H == 1 ? 8 : H == 2 ? 4 : H <= 4 ? 2 : 1;  // waves per sender head
 
-  // ---- stage the tile's alignment entries ----
   if (tid <= 64) estart[tid] = p.row_ptr[g0 + min(tid, nrows)];
-  if (tid == 0) flag[0] = p.s_extent > 0 ? 0 : 1;
-  if (unrot) {  // U(0..15): rows 0..15 of the sender table, 2 per wave
-    const int ri = wave * 2 + (lane >> 5);
-    const int c = (lane & 31) ^ (ri & 1);
-    copy16_to_lds(p.cs_s + (long long)ri * kDH + 4 * c, dt + wave * 2 * kDH);
-  }
+  if (tid < 4) flag[tid] = 0;
   __syncthreads();
   const int e_base = estart[0];
   const int nnz = estart[nrows] - e_base;
-  bool staged = nnz <= kEMax;
-  if (staged) {
-    for (int t = tid; t < nnz; t += 512) {
-      int lo = 0, hi = nrows;  // row r with estart[r] <= e_base + t < estart[r + 1]
+  const bool fits = nnz <= kEMax;
+  if (fits) {
+    for (int k = tid; k < nnz; k += 512) {
+      int lo = 0, hi = nrows;  // row r with estart[r] <= e_base + k < estart[r + 1]
       while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if (estart[mid] <= e_base + t) lo = mid; else hi = mid;
+        if (estart[mid] <= e_base + k) lo = mid; else hi = mid;
       }
-      const int e = e_base + t;
-      ecol[t] = min(max(p.col[e], 0), cx.Ts - 1);
-      ew[t] = (float)p.num[e] / (float)p.den[g0 + lo];
-      einfo[t] = lo | ((int)(e + 1 == estart[lo + 1]) << 8);
+      const int e = e_base + k;
+      ecol[k] = min(max(p.col[e], 0), Ts - 1);
+      ew[k] = (float)p.num[e] / (float)p.den[g0 + lo];
+      einfo[k] = lo | ((int)(e + 1 == estart[lo + 1]) << 8) | ((int)(e == estart[lo]) << 9);
     }
   }
   __syncthreads();
   const int NG = 8 * WPH;  // lane groups over the tile's rows
   if (wave == 0) {
-    // Contiguous runs of rows with equal shares of the tile's entries: the
-    // build of a wave takes as many trips as its longest run.
     if (lane <= NG) {
-      int b = lane == NG ? 64 : 0;
+      int bnd = lane == NG ? 64 : 0;
       if (lane > 0 && lane < NG) {
         const int target = (lane * nnz + NG / 2) / NG;
         int lo = 0, hi = nrows;  // smallest r with estart[r] - e_base >= target
@@ -580,12 +583,12 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
           const int mid = (lo + hi) >> 1;
           if (estart[mid] - e_base >= target) hi = mid; else lo = mid + 1;
         }
-        b = lo;
+        bnd = lo;
       }
-      gstart[lane] = b;
+      gstart[lane] = bnd;
     }
     int lmin = INT_MAX, lmax = -1;  // lane = tile row
-    if (staged)
+    if (fits && lane < nrows)
       for (int k = estart[lane] - e_base; k < estart[lane + 1] - e_base; ++k) {
         lmin = min(lmin, ecol[k]);
         lmax = max(lmax, ecol[k]);
@@ -599,12 +602,54 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
         gmax = max(gmax, rmax[r]);
       }
       gbase[lane] = gmax < 0 ? 0 : gmin;
-      if (unrot && gmax >= 0 && gmax - gmin >= kDMax) flag[0] = 1;
+      if (gmax >= 0 && gmax - gmin >= kDMax) flag[0] = 1;
     }
+    if (lane == 0 && !fits) flag[1] = 1;
   }
-  __builtin_amdgcn_s_waitcnt(0);  // the rotation table has landed
   __syncthreads();
-  staged = staged && flag[0] == 0;
+  int4* dst = reinterpret_cast<int4*>(rec + (long long)t * (kRecBytes / 4));
+  dst[tid] = reinterpret_cast<const int4*>(ent)[tid];
+}
+
+template <int NTW, bool MULTI>
+__global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const TransferArgs p) {
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kSmemBytes];
+  uint16_t* Xs = reinterpret_cast<uint16_t*>(smem);
+  float* dt = reinterpret_cast<float*>(smem + kOffDt);
+  int* estart = reinterpret_cast<int*>(smem + kOffEnt);
+  int* gbase = estart + 65;
+  int* ecol = gbase + 64;
+  float* ew = reinterpret_cast<float*>(ecol + kEMax);
+  int* einfo = reinterpret_cast<int*>(ew + kEMax);
+  const int* flag = einfo + kEMax;  // [0] a run too wide for U(0..15), [1] too many entries
+  const int* gstart = flag + 4;     // lane group g walks tile rows [gstart[g], gstart[g + 1])
+
+  const Item it = decode_item(p, blockIdx.x);
+  const Ctx cx = make_ctx(p, it);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int Tr = p.Tr[it.b];
+  const int j0 = it.tile * 64;
+  const int nrows = min(64, Tr - j0);
+  const int g0 = p.row0[it.b] + j0;
+  const bool unrot = cx.cs_s != nullptr;
+  const int H = p.H_s;
+  // WPH waves share a sender head; each lane group walks a run of rows
+  const int WPH = H == 1 ? 8 : H == 2 ? 4 : H <= 4 ? 2 : 1;
+
+  // ---- stage: the tile's record and the rotation table ----
+  {
+    const int* rec = p.tile_rec + (long long)(p.tile_start[it.b] + it.tile) * (kRecBytes / 4);
+    copy16_to_lds(rec + wave * 256 + 4 * lane, estart + wave * 256);
+  }
+  if (unrot) {  // U(0..15): rows 0..15 of the sender table, 2 per wave
+    const int ri = wave * 2 + (lane >> 5);
+    const int c = (lane & 31) ^ (ri & 1);
+    copy16_to_lds(p.cs_s + (long long)ri * kDH + 4 * c, dt + wave * 2 * kDH);
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // both copies have landed
+  __syncthreads();
+  const int e_base = estart[0];
+  const bool staged = p.s_extent > 0 && flag[1] == 0 && !(unrot && flag[0] != 0);
 
   f32x16 acc[2][NTW];  // zeroed after the first tap's build
   // This wave's accumulators: receiver head `head`, n-tiles feat[q].
@@ -1041,6 +1086,23 @@ int transfer_rows_per_tile(int dtype, int H_r, int H_s, int n_taps, int d_h) {
   const int d_in = n_taps * H_s * d_h;
   int rt = 8192 / (d_in > 0 ? d_in : 1);  // fp32 X tile <= 32 KB of LDS
   return rt < 1 ? 1 : (rt > 16 ? 16 : rt);
+}
+
+static bool uses_tiled(int dtype, int H_r, int H_s, int d_h) {
+  return dtype == HF_BF16 && d_h == kDH && (H_r == 4 || H_r == 8) && H_s <= kHMax;
+}
+
+size_t transfer_tile_record_bytes(int dtype, int H_r, int H_s, int d_h) {
+  return uses_tiled(dtype, H_r, H_s, d_h) ? kRecBytes : 0;
+}
+
+hipError_t launch_transfer_stage(int dtype, const TransferArgs& a, hipStream_t s) {
+  const int tiles = a.tile_start[a.B];
+  if (!uses_tiled(dtype, a.H_r, a.H_s, a.d_h) || tiles <= 0) return hipSuccess;
+  if (!a.tile_rec) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(stage_tiles_kernel, dim3((unsigned)tiles), dim3(512), 0, s, a,
+                     const_cast<int*>(a.tile_rec));
+  return hipGetLastError();
 }
 
 hipError_t launch_rope_table(float* tab, int P, int d_h, double theta, hipStream_t s) {

@@ -31,6 +31,7 @@ HF_LAYERS_INTERP2 = 0
 HF_F32, HF_BF16 = 0, 1
 HF_KERNEL_TRANSFER, HF_KERNEL_ROPE_TABLES, HF_KERNEL_ALIGNMENT, HF_KERNEL_PACK = 0, 1, 2, 3
 HF_KERNEL_MOMENTS_STATS, HF_KERNEL_MOMENTS_COV, HF_KERNEL_RECOLOR_SOLVE, HF_KERNEL_FOLD = 4, 5, 6, 7
+HF_KERNEL_TRANSFER_STAGE = 8
 HF_MAX_BATCH = 64
 ALIGN_MODES = {"overlap": HF_ALIGN_OVERLAP, "ta": HF_ALIGN_TA}
 

@@ -151,9 +151,42 @@ def test_transfer_host_validation(L):
     assert call(opts=hf.hf_transfer_opts(C.c_void_p(0x1002), None, 0.0)) == -2      # misaligned
     assert call(sd=_desc(dtype=0, d=96), rd=_desc(L_=6, dtype=0, d=96),
                 opts=hf.hf_transfer_opts(None, C.c_void_p(0x1000), 1e-6)) == -8   # fp32 norm d_h
-    # cos/sin tables: 64 sender + 60 receiver positions x 64 pairs x 8 bytes
+    # cos/sin tables: 64 sender + 60 receiver positions x 64 pairs x 8 bytes, then
+    # one 8 KB staging record per 64-row receiver tile
     assert L.hf_transfer_workspace_bytes(1, _p(s_len), _p(r_len), C.byref(_desc()),
-                                         C.byref(_desc(L_=6)), C.byref(r)) == 64 * 512 + 60 * 512
+                                         C.byref(_desc(L_=6)), C.byref(r)) == 64 * 512 + 60 * 512 + 8192
+
+
+def test_transfer_workspace_records(L):
+    s_len = np.array([64, 64, 64], np.int32)
+    r_len = np.array([60, 0, 64], np.int32)
+    lt = [np.ascontiguousarray(x, dtype=np.int32) for x in lm.interp2(4, 6)]
+    fake = C.c_void_p(0x1000)
+
+    def wsb(sd, rd):
+        return L.hf_transfer_workspace_bytes(3, _p(s_len), _p(r_len), C.byref(sd), C.byref(rd), None)
+
+    # bf16 with 8 or 4 receiver heads: one record per non-empty 64-row tile
+    assert wsb(_desc(), _desc(L_=6)) == 2 * 8192
+    assert wsb(_desc(H=4), _desc(L_=6, H=4)) == 2 * 8192
+    r130 = np.array([130], np.int32)
+    assert L.hf_transfer_workspace_bytes(1, _p(np.array([200], np.int32)), _p(r130),
+                                         C.byref(_desc(T=256)), C.byref(_desc(L_=6, T=256)),
+                                         None) == 3 * 8192
+    # kernels that keep no records: 2 receiver heads, more than 8 sender heads, fp32
+    assert wsb(_desc(), _desc(L_=6, H=2)) == 0
+    assert wsb(_desc(H=16), _desc(L_=6)) == 0
+    assert wsb(_desc(dtype=0), _desc(L_=6, dtype=0)) == 0
+
+    def call(ws, n):
+        sd, rd = _desc(), _desc(L_=6)
+        return L.hf_transfer_kv(3, _p(s_len), _p(r_len), fake, fake, fake, fake,
+                                *[_p(t) for t in lt], C.byref(sd), C.byref(rd), fake, None,
+                                None, None, ws, n, None)
+
+    assert call(None, 0) == -1                       # records need a workspace
+    assert call(C.c_void_p(0x100000), 8192) == -6    # too small
+    assert call(C.c_void_p(0x100000 + 16), 1 << 20) == -2   # not 256-byte aligned
 
 
 def test_pack_host_validation(L):
