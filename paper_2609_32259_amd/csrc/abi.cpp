@@ -429,6 +429,8 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
     const int H = receiver->H;
     if (H != 2 && H != 4 && H != 8)
       return fail(HF_ERR_UNSUPPORTED, "bf16 path needs receiver H in {2,4,8} (got %d)", H);
+    if ((int64_t)H * d_h * d_all * 2 >= ((int64_t)1 << 31))
+      return fail(HF_ERR_UNSUPPORTED, "bf16 path needs one (layer, role) map under 2 GiB");
   } else if (d_all > 4096 || d_in % 4) {
     return fail(HF_ERR_UNSUPPORTED, "fp32 path needs n_taps*d_in <= 4096 and d_in %% 4 == 0");
   }

@@ -722,15 +722,22 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
     }
 
     // ---- multiply ----
-    const bf16x8* W = static_cast<const bf16x8*>(p.Wp) +
-                      ((long long)lc_store * p.n_taps + tap) * KS * NB * 64 + (4 * head + nt0) * 64 +
-                      lane;
+    // The map block of this (layer, role, tap) through a buffer resource: a
+    // 32-bit per-lane offset plus the k-step's scalar offset, so a refill costs
+    // no 64-bit address arithmetic.
+    const bf16x8* Wblk =
+        static_cast<const bf16x8*>(p.Wp) + ((long long)lc_store * p.n_taps + tap) * KS * NB * 64;
+    const __amdgpu_buffer_rsrc_t rW =
+        __builtin_amdgcn_make_buffer_rsrc((void*)Wblk, 0, KS * NB * 64 * 16, 0x00020000);
+    const int w_lane = ((4 * head + nt0) * 64 + lane) * 16;  // bytes within a k-step
     bf16x8 wr[4][NTW];  // map fragments of four consecutive k-steps
     auto kstep = [&](int ks) { int k = ks + ks0; return k >= KS ? k - KS : k; };
     auto load_w = [&](bf16x8* dst, int ks) {
-      const bf16x8* Wk = W + (long long)kstep(ks) * NB * 64;
+      const int k_off = kstep(ks) * NB * 64 * 16;
 #pragma unroll
-      for (int q = 0; q < NTW; ++q) dst[q] = Wk[q * NTS * 64];
+      for (int q = 0; q < NTW; ++q)
+        dst[q] = __builtin_bit_cast(
+            bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rW, w_lane + q * NTS * 64 * 16, k_off, 0));
     };
     auto read_x = [&](bf16x8* xa, int ks) {
       const int k = kstep(ks);
@@ -895,8 +902,11 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_direct_kernel(const Tran
   const int KS = p.n_taps * p.H_s * (kDH / 16);  // k-steps of the whole map row
   const int NB = p.H_r * (kDH / 32);
   const int lc_store = it.l * 2 + it.c;
-  const bf16x8* W = static_cast<const bf16x8*>(p.Wp) + (long long)lc_store * KS * NB * 64 +
-                    (wn * 4) * 64 + lane;
+  // Map fragments through a buffer resource over this (layer, role)'s block.
+  const __amdgpu_buffer_rsrc_t rW = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(static_cast<const bf16x8*>(p.Wp) + (long long)lc_store * KS * NB * 64), 0,
+      KS * NB * 64 * 16, 0x00020000);
+  const int w_lane = ((wn * 4) * 64 + lane) * 16;  // bytes
   const int brow = tid >> 3;
   const int e0 = (tid & 7) * 8;
 
@@ -924,7 +934,7 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_direct_kernel(const Tran
       *reinterpret_cast<uint4*>(xb + r * kXS + e0 + 64) = pack8(x + 8);
     }
     __syncthreads();
-    const bf16x8* Wh = W + (long long)v * 8 * NB * 64;
+    const int v_off = v * 8 * NB * 64 * 16;  // k-steps of block v
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       bf16x8 xa[2], wf[4];
@@ -933,7 +943,9 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_direct_kernel(const Tran
         xa[mt] = *reinterpret_cast<const bf16x8*>(
             xb + (64 * wm + 32 * mt + (lane & 31)) * kXS + 16 * s + 8 * (lane >> 5));
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) wf[nt] = Wh[(s * NB + nt) * 64];
+      for (int nt = 0; nt < 4; ++nt)
+        wf[nt] = __builtin_bit_cast(
+            bf16x8, __builtin_amdgcn_raw_buffer_load_b128(rW, w_lane + (s * NB + nt) * 64 * 16, v_off, 0));
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
