@@ -684,18 +684,18 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
         const int base = gbase[grp];
         if (MULTI) {  // one sender layer per tap
           if (tap == 0) {
-            if (unrot) build_groups<false, true, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
-            else build_groups<false, false, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+            if (unrot) build_groups<false, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+            else build_groups<false, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
           } else {
             if (unrot) build_groups<false, true, 2>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
             else build_groups<false, false, 2>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
           }
         } else if (ct.two_tap) {
-          if (unrot) build_groups<true, true, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
-          else build_groups<true, false, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+          if (unrot) build_groups<true, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+          else build_groups<true, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
         } else {
-          if (unrot) build_groups<false, true, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
-          else build_groups<false, false, 4>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+          if (unrot) build_groups<false, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+          else build_groups<false, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
         }
       }
     } else {
