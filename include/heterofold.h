@@ -33,7 +33,9 @@
  *  - All host-checkable arguments are validated before anything is launched.
  *    Device-side data that cannot be checked on the host (character offsets,
  *    CSR contents) never causes an out-of-bounds access: indices are clamped
- *    into the buffers the sizes describe.
+ *    into the buffers the sizes describe.  The one exception is the CSR row
+ *    offsets the transfer calls read, which they trust: they must be the table
+ *    hf_build_alignment wrote (always monotone and within its capacity).
  *  - Character spans: token t of a sequence covers characters [beg[t], end[t]).
  *    Valid spans are sorted and non-overlapping: 0 <= beg[t] <= end[t] <=
  *    beg[t+1].  Empty tokens (beg == end) and gaps are allowed.  Results for
@@ -254,7 +256,8 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  * Arguments
  *   s_len, r_len   host int32 [B]: token counts (<= sender/receiver T_cap).
  *   row_ptr, col, num, den   device: the table hf_build_alignment wrote for
- *                  the same batch (row r_cu[b]+j as documented there).
+ *                  the same batch (row r_cu[b]+j as documented there).  col is
+ *                  clamped into the sequence; row_ptr is trusted (see above).
  *   lo, hi, rem, den_l       host int32 [receiver->L]: hf_build_layer_map's table.
  *   sender, receiver         cache descriptors; same dtype and d_h.
  *                  receiver->L is L_r; d_in = sender->H*d_h, d_r = receiver->H*d_h.
