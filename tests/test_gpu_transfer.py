@@ -52,11 +52,11 @@ def _oracle_seq(wl, b, mode, rope):
                        H_r=cfg.H_r)
 
 
-def _compare_full(torch, cfg, wl, mode="overlap", rope="cfg", qlimited_k=False):
+def _compare_full(torch, cfg, wl, mode="overlap", rope="cfg", qlimited_k=False, R=None):
     rope = wl.rope if rope == "cfg" else rope
     print(f"[gpu-transfer] {cfg.name} mode={mode} B={wl.seg.batch} T_s={list(wl.seg.s_len)} "
           f"T_r={list(wl.seg.r_len)} rope={rope is not None}", flush=True)
-    path = _path(cfg, wl, mode, rope)
+    path = _path(cfg, wl, mode, rope, R=R)
     R = path.step()
     torch.cuda.synchronize()
     worst = (0.0, 0.0)
@@ -133,6 +133,35 @@ def test_bf16_reverse_batched_ragged(torch):
                              pos0_r=np.array([2, 0, 11, 70], np.int32))
     wl = synth.Workload(cfg, seg, S, A, bias, rope)
     _compare_full(torch, cfg, wl, "overlap")
+
+
+@pytest.mark.parametrize("H_r", [8, 4])
+def test_bf16_batch_with_empty_sequences(torch, H_r):
+    # A sequence with no tokens and one with sender tokens but no receiver
+    # tokens own no row tiles (and no staging records); the sequences around
+    # them still map correctly, and no receiver row outside the lengths changes.
+    cfg = synth.LLAMA8B_14B_8K.with_(name=f"empty sequences H_r={H_r}", H_r=H_r, L_r=3)
+    rng = np.random.default_rng(12)
+    parts = []
+    for n_s, with_r in ((0, False), (150, True), (40, False), (90, True)):
+        sb, se = synth.segment_tokens(rng, n_s, 1, 7)
+        n_chars = int(se[-1]) if n_s and with_r else 0
+        rb, re_ = synth.segment_chars(rng, n_chars, 1, 8)
+        parts.append((sb, se, rb, re_))
+    seg = synth.concat_segmentations(parts)
+    assert list(seg.r_len == 0) == [True, False, True, False]
+    S = synth.make_cache(cfg, seg, seed=12, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=12, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=np.array([0, 5, 9, 300], np.int32),
+                             pos0_r=np.array([0, 2, 0, 40], np.int32))
+    wl = synth.Workload(cfg, seg, S, A, bias, rope)
+    T_cap = int(seg.r_len.max()) + 21
+    R = torch.full((4, cfg.L_r, 2, cfg.H_r, T_cap, cfg.d_h), 3.0, dtype=torch.bfloat16,
+                   device="cuda")
+    _compare_full(torch, cfg, wl, "overlap", R=R)
+    for b in range(4):
+        T_r = int(seg.r_len[b])
+        assert bool((R[b, :, :, :, T_r:, :] == 3.0).all()), f"sequence {b}: rows past {T_r} changed"
 
 
 @pytest.mark.parametrize("H_r", [8, 4])
