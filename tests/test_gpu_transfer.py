@@ -188,6 +188,26 @@ def test_bf16_tiles_beyond_staging_capacity(torch, H_r):
     _compare_full(torch, cfg, wl, "overlap")
 
 
+@pytest.mark.parametrize("H_r", [8, 4])
+def test_bf16_runs_too_wide_for_the_rotation_table(torch, H_r):
+    # One-character sender tokens under 4-6 character receiver tokens: about 5
+    # entries per row, so a tile stays within the staged entry count, but a run
+    # of rows spans more sender positions than the in-LDS rotation table holds.
+    # Key tiles then build from global memory while value tiles stay staged.
+    cfg = synth.LLAMA8B_14B_8K.with_(name=f"wide runs H_r={H_r}", H_r=H_r, L_r=3)
+    rng = np.random.default_rng(13)
+    sb, se = synth.segment_tokens(rng, 1500, 1, 1)
+    rb, re_ = synth.segment_chars(rng, int(se[-1]), 4, 6)
+    seg = synth.concat_segmentations([(sb, se, rb, re_)])
+    row_ptr, col, _, _ = al.build_alignment(sb, se, rb, re_, "overlap")
+    assert np.diff(row_ptr[::64]).max() <= 512          # every tile's entries are staged
+    assert col[row_ptr[8]] - col[0] >= 16               # a run of 8 rows spans 16+ tokens
+    S = synth.make_cache(cfg, seg, seed=13, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=13, device="cuda")
+    wl = synth.Workload(cfg, seg, S, A, bias, synth.rope_params(cfg, pos0_s=np.array([3], np.int32)))
+    _compare_full(torch, cfg, wl, "overlap")
+
+
 def test_bf16_two_receiver_heads(torch):
     cfg = synth.LLAMA8B_14B_8K.with_(name="8->2 heads", H_r=2, L_r=3, T_s=700)   # 256-row tiles
     wl = synth.make_workload(cfg, seed=5, device="cuda")
