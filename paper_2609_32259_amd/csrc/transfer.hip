@@ -50,17 +50,22 @@ __device__ __forceinline__ void copy16_to_lds(const void* gsrc, void* lds_wave_b
 // RoPE tables: row pos holds cos(pos w_k) for k < d/2, then sin(pos w_k), with
 // w_k = theta^(-2k/d); the angle is formed in fp64.
 // ---------------------------------------------------------------------------
+// A thread owns one angle index k (threadIdx.x + 64 blockIdx.y) and kRopePpt
+// consecutive positions, so w_k is formed once per thread.
+constexpr int kRopePpt = 16;
 __global__ __launch_bounds__(256) void rope_table_kernel(float* tab, int P, int half, int d,
                                                          double theta) {
-  const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (long long)P * half) return;
-  const int pos = (int)(idx / half), k = (int)(idx % half);
+  const int k = blockIdx.y * 64 + threadIdx.x;
+  if (k >= half) return;
   const double w = pow(theta, -2.0 * k / d);
-  const double ang = (double)pos * w;
-  double s, c;
-  sincos(ang, &s, &c);
-  tab[(long long)pos * d + k] = (float)c;
-  tab[(long long)pos * d + half + k] = (float)s;
+  const long long p0 = ((long long)blockIdx.x * 4 + threadIdx.y) * kRopePpt;
+  const int p1 = (int)min(p0 + kRopePpt, (long long)P);
+  for (int pos = (int)min(p0, (long long)P); pos < p1; ++pos) {
+    double s, c;
+    sincos((double)pos * w, &s, &c);
+    tab[(long long)pos * d + k] = (float)c;
+    tab[(long long)pos * d + half + k] = (float)s;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1121,8 +1126,8 @@ hipError_t launch_rope_table(float* tab, int P, int d_h, double theta, hipStream
   const int half = d_h / 2;
   const long long n = (long long)P * half;
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, tab, P,
-                     half, d_h, theta);
+  const dim3 grid((unsigned)((P + 4 * kRopePpt - 1) / (4 * kRopePpt)), (unsigned)((half + 63) / 64));
+  hipLaunchKernelGGL(rope_table_kernel, grid, dim3(64, 4), 0, s, tab, P, half, d_h, theta);
   return hipGetLastError();
 }
 
