@@ -275,7 +275,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the transfer path is built and timed on a single "
-              f"MI355X; --gpus {args.gpus} is not supported (how it would shard is in DESIGN.md)",
+              f"MI355X; --gpus {args.gpus} is not supported",
               file=sys.stderr)
         sys.exit(2)
 

@@ -64,7 +64,7 @@ typedef enum {
   HF_ERR_DTYPE = -5,       /* unknown or mismatched storage type */
   HF_ERR_CAPACITY = -6,    /* an output or workspace buffer is too small */
   HF_ERR_HIP = -7,         /* a HIP runtime call or kernel launch failed */
-  HF_ERR_UNSUPPORTED = -8  /* a valid shape this build has no kernel for */
+  HF_ERR_UNSUPPORTED = -8  /* a valid shape the library has no kernel for */
 } hf_status;
 
 typedef enum { HF_ALIGN_OVERLAP = 0, HF_ALIGN_TA = 1 } hf_align_mode;
@@ -270,7 +270,7 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  * rounds it once to bf16 (round-to-nearest-even), multiplies on the matrix
  * cores with fp32 accumulation, adds bias and rotates in fp32, and rounds the
  * result once to bf16.
- * Supported by this build: d_h == 128 for HF_BF16 with receiver H in
+ * Supported by this library: d_h == 128 for HF_BF16 with receiver H in
  * {2, 4, 8} and one (layer, role) map under 2 GiB; any even d_h and H for
  * HF_F32 (d_in <= 4096).  Other valid
  * shapes return HF_ERR_UNSUPPORTED.  Receiver rows past r_len are not written.
