@@ -237,7 +237,8 @@ int32_t hf_pack_maps(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype, cons
  * cos/sin tables (none without RoPE) and, for bf16 with 4 or 8 receiver heads
  * and at most 8 sender heads, an 8 KB staging record per 64-row receiver tile
  * (the tile's alignment entries, written once per call and read by every
- * receiver layer and role).  0 when neither applies.
+ * receiver layer and role) plus 256 bytes for a work counter.  0 when neither
+ * applies.  Calls that share a workspace must not overlap.
  */
 size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
                                    const hf_kv_desc* sender, const hf_kv_desc* receiver,

@@ -357,8 +357,8 @@ int32_t rope_sizes(int32_t B, const int32_t* s_len, const int32_t* r_len, const 
 
 size_t rope_bytes(int P, int d_h) { return align_up((size_t)P * d_h * sizeof(float), 256); }
 
-// Staging records of the row tiles (one per tile of the batch), where the
-// kernel that runs keeps them.
+// Staging records of the row tiles (one per tile of the batch) and the work
+// counter after them, where the kernel that runs keeps them.
 size_t record_bytes(int32_t B, const int32_t* r_len, const hf_kv_desc* sender,
                     const hf_kv_desc* receiver) {
   const size_t per = hf::transfer_tile_record_bytes(sender->dtype, receiver->H, sender->H,
@@ -367,7 +367,7 @@ size_t record_bytes(int32_t B, const int32_t* r_len, const hf_kv_desc* sender,
   const int rt = hf::transfer_rows_per_tile(sender->dtype, receiver->H, sender->H, 1, sender->d_h);
   size_t tiles = 0;
   for (int b = 0; b < B; ++b) tiles += r_len[b] > 0 ? ((size_t)r_len[b] + rt - 1) / rt : 0;
-  return tiles * per;
+  return tiles * per + 256;
 }
 
 }  // namespace
@@ -554,8 +554,18 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
     a.cs_r = reinterpret_cast<const float*>(w + rope_bytes(rs.P_s, d_h));
     a.rot = 1;
   }
-  if (ws_need > rec_off) a.tile_rec = reinterpret_cast<const int32_t*>(w + rec_off);
+  if (ws_need > rec_off) {
+    a.tile_rec = reinterpret_cast<const int32_t*>(w + rec_off);
+    a.work_ctr = reinterpret_cast<int32_t*>(w + ws_need - 256);
+  }
   if (tiles == 0) return ok();
+  if (a.tile_rec) {
+    int dev = 0, n_cu = 0;
+    hipError_t de = hipGetDevice(&dev);
+    if (de == hipSuccess) de = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (de != hipSuccess) return hip_fail(de, "device query");
+    a.n_wg = hf::transfer_persistent_grid(a, n_cu > 0 ? n_cu : 1);
+  }
   hipError_t e = hipSuccess;
   if (a.unrot || a.rot) {
     TimedLaunch t(HF_KERNEL_ROPE_TABLES, s);

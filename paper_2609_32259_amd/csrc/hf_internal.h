@@ -51,6 +51,8 @@ struct TransferArgs {
   const int32_t* num;
   const int32_t* den;
   const int32_t* tile_rec;  // per-row-tile staging records (tiled bf16 kernel)
+  int32_t* work_ctr;        // next work item of the persistent tiled kernel
+  int32_t n_wg;             // workgroups of the persistent tiled kernel
   const float* cs_s;    // sender RoPE table [P_s][d_h]: cos of the d_h/2 angles, then sin
   const float* cs_r;    // receiver RoPE table [P_r][d_h], same layout
   const float* inv_r;   // [L_r][2] scalar 1/r per layer and role, or nullptr (1)
@@ -86,6 +88,8 @@ int transfer_rows_per_tile(int dtype, int H_r, int H_s, int n_taps, int d_h);
 // that runs keeps no records), and the launch that writes the records
 // (a.tile_rec, one per tile of the batch) before launch_transfer.
 size_t transfer_tile_record_bytes(int dtype, int H_r, int H_s, int d_h);
+// Workgroups of the persistent tiled kernel on a device with n_cu compute units.
+int transfer_persistent_grid(const TransferArgs& a, int n_cu);
 hipError_t launch_transfer_stage(int dtype, const TransferArgs& a, hipStream_t s);
 
 hipError_t launch_alignment(const AlignArgs& a, hipStream_t s);

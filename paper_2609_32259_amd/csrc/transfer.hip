@@ -353,7 +353,8 @@ constexpr int kOffEnt = kOffDt + kDtBytes;
 constexpr int kEntInts = 65 + 64 + kEMax * 3 + 4 + 65 + 2 * 64;
 constexpr int kRecBytes = 8192;  // 8 waves x 64 lanes x 16 bytes
 static_assert(kEntInts * 4 <= kRecBytes, "tile record size");
-constexpr int kSmemBytes = kOffEnt + kRecBytes;
+constexpr int kOffNext = kOffEnt + kRecBytes;  // the workgroup's next work item
+constexpr int kSmemBytes = kOffNext + 16;
 // Store phase, inside the (then free) X region: receiver RoPE rows, bias, staging.
 constexpr int kOffRcs = 0;                           // [64][cos 64 | sin 64] fp32
 constexpr int kOffBias = kOffRcs + 64 * kDH * 4;     // [d_r <= 1024] fp32
@@ -535,6 +536,7 @@ __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& 
 // role) of the tile reads the same record.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(512) void stage_tiles_kernel(const TransferArgs p, int* rec) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) *p.work_ctr = p.n_wg;  // items [0, n_wg) start statically
   __shared__ __attribute__((aligned(16))) int ent[kRecBytes / 4];
   int* estart = ent;
   int* gbase = estart + 65;
@@ -628,33 +630,49 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   int* einfo = reinterpret_cast<int*>(ew + kEMax);
   const int* flag = einfo + kEMax;  // [0] a run too wide for U(0..15), [1] too many entries
   const int* gstart = flag + 4;     // lane group g walks tile rows [gstart[g], gstart[g + 1])
+  int* next_item = reinterpret_cast<int*>(smem + kOffNext);
 
-  const Item it = decode_item(p, blockIdx.x);
-  const Ctx cx = make_ctx(p, it);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int Tr = p.Tr[it.b];
-  const int j0 = it.tile * 64;
-  const int nrows = min(64, Tr - j0);
-  const int g0 = p.row0[it.b] + j0;
-  const bool unrot = cx.cs_s != nullptr;
   const int H = p.H_s;
   // WPH waves share a sender head; each lane group walks a run of rows
   const int WPH = H == 1 ? 8 : H == 2 ? 4 : H <= 4 ? 2 : 1;
-
-  // ---- stage: the tile's record and the rotation table ----
-  {
-    const int* rec = p.tile_rec + (long long)(p.tile_start[it.b] + it.tile) * (kRecBytes / 4);
+  const int n_items = p.tiles_per_lc * p.L_r * 2;
+  // The tile's staging record into LDS, one 16-byte-per-lane copy per wave.
+  auto copy_record = [&](int item) {
+    const Item ni = decode_item(p, item);
+    const int* rec = p.tile_rec + (long long)(p.tile_start[ni.b] + ni.tile) * (kRecBytes / 4);
     copy16_to_lds(rec + wave * 256 + 4 * lane, estart + wave * 256);
-  }
-  if (unrot) {  // U(0..15): rows 0..15 of the sender table, 2 per wave
+  };
+
+  // Persistent (interpolating map): the workgroup starts on work item
+  // blockIdx.x and takes the next one from the work counter (set to the grid
+  // size by the staging kernel) while it builds, so the items in flight stay a
+  // contiguous run of the work order, and the next record is copied in during
+  // the store.  With concatenated taps (whose per-tap passes leave no registers
+  // for the loop) a workgroup does the one item blockIdx.x.
+  constexpr bool kPersist = !MULTI;
+  int item = blockIdx.x;
+  copy_record(item);
+  if (p.unrot) {  // U(0..15): rows 0..15 of the sender table, 2 per wave
     const int ri = wave * 2 + (lane >> 5);
     const int c = (lane & 31) ^ (ri & 1);
     copy16_to_lds(p.cs_s + (long long)ri * kDH + 4 * c, dt + wave * 2 * kDH);
   }
   __builtin_amdgcn_s_waitcnt(0);  // both copies have landed
   __syncthreads();
+
+  for (;;) {
+  const Item it = decode_item(p, item);
+  const Ctx cx = make_ctx(p, it);
+  const int Tr = p.Tr[it.b];
+  const int j0 = it.tile * 64;
+  const int nrows = min(64, Tr - j0);
+  const int g0 = p.row0[it.b] + j0;
+  const bool unrot = cx.cs_s != nullptr;
   const int e_base = estart[0];
   const bool staged = p.s_extent > 0 && flag[1] == 0 && !(unrot && flag[0] != 0);
+  int grabbed = n_items;
+  if (kPersist && tid == 0) grabbed = atomicAdd(p.work_ctr, 1);
 
   f32x16 acc[2][NTW];  // zeroed after the first tap's build
   // This wave's accumulators: receiver head `head`, n-tiles feat[q].
@@ -667,7 +685,7 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   const int KS = H * (kDH / 16);  // k-steps of one tap
   const int NB = p.H_r * (kDH / 32);
   const int lc_store = it.l * 2 + it.c;
-  const int ks0 = (int)(blockIdx.x % (unsigned)H) * (kDH / 16);  // this workgroup's first k-step
+  const int ks0 = (int)((unsigned)item % (unsigned)H) * (kDH / 16);  // this item's first k-step
 
   // One pass per tap of the layer map (MULTI: concatenated taps, each one
   // sender layer): build that tap's X, multiply it by the matching k block of
@@ -783,7 +801,9 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
     step(wr[2], KS - 2, NoLoad());
     step(wr[3], KS - 1, NoLoad());
   }
+  if (tid == 0) *next_item = grabbed;
   __syncthreads();  // every wave is done reading X; the X region is free
+  const int next = *next_item;
 
   // ---- store ----
   const bool rot = it.c == 0 && p.rot;
@@ -802,6 +822,7 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   }
   if (p.bias && wave < d_r / 256)  // 256 floats per wave instruction
     copy16_to_lds(p.bias + (long long)lc_store * d_r + wave * 256 + 4 * lane, bias_s + wave * 256);
+  if (next < n_items) copy_record(next);  // this item's record is no longer read
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
@@ -880,6 +901,10 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
       if (jj < Tr)
         *reinterpret_cast<uint4*>(dst_head + (long long)jj * p.r_st + feat[ci / 4] + 8 * (ci % 4)) = v;
     }
+  }
+  if (!kPersist || next >= n_items) break;
+  __syncthreads();  // every wave is done with the staging rows; the next build writes X
+  item = next;
   }
 }
 
@@ -1113,10 +1138,16 @@ size_t transfer_tile_record_bytes(int dtype, int H_r, int H_s, int d_h) {
   return uses_tiled(dtype, H_r, H_s, d_h) ? kRecBytes : 0;
 }
 
+int transfer_persistent_grid(const TransferArgs& a, int n_cu) {
+  const long long items = (long long)a.tiles_per_lc * a.L_r * 2;
+  return (int)(items < n_cu ? items : n_cu);
+}
+
 hipError_t launch_transfer_stage(int dtype, const TransferArgs& a, hipStream_t s) {
   const int tiles = a.tile_start[a.B];
   if (!uses_tiled(dtype, a.H_r, a.H_s, a.d_h) || tiles <= 0) return hipSuccess;
   if (!a.tile_rec) return hipErrorInvalidValue;
+  if (!a.work_ctr || a.n_wg < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(stage_tiles_kernel, dim3((unsigned)tiles), dim3(512), 0, s, a,
                      const_cast<int*>(a.tile_rec));
   return hipGetLastError();
@@ -1151,21 +1182,24 @@ hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s) {
   const long long items = (long long)a.tiles_per_lc * a.L_r * 2;
   if (items <= 0) return hipSuccess;
   const dim3 grid((unsigned)items);
+  const bool tiled = uses_tiled(dtype, a.H_r, a.H_s, a.d_h);
+  if (tiled && (!a.tile_rec || !a.work_ctr || a.n_wg < 1)) return hipErrorInvalidValue;
+  const dim3 pgrid((unsigned)a.n_wg);  // persistent (interpolating map): one workgroup per CU
   if (dtype == HF_BF16) {
     switch (a.H_r) {
       case 2: hipLaunchKernelGGL(transfer_bf16_direct_kernel<2>, grid, dim3(512), 0, s, a); break;
       case 4:
-        if (a.H_s <= kHMax && a.concat)
+        if (tiled && a.concat)
           hipLaunchKernelGGL((transfer_bf16_tiled_kernel<2, true>), grid, dim3(512), 0, s, a);
-        else if (a.H_s <= kHMax)
-          hipLaunchKernelGGL((transfer_bf16_tiled_kernel<2, false>), grid, dim3(512), 0, s, a);
+        else if (tiled)
+          hipLaunchKernelGGL((transfer_bf16_tiled_kernel<2, false>), pgrid, dim3(512), 0, s, a);
         else hipLaunchKernelGGL(transfer_bf16_direct_kernel<4>, grid, dim3(512), 0, s, a);
         break;
       case 8:
-        if (a.H_s <= kHMax && a.concat)
+        if (tiled && a.concat)
           hipLaunchKernelGGL((transfer_bf16_tiled_kernel<4, true>), grid, dim3(512), 0, s, a);
-        else if (a.H_s <= kHMax)
-          hipLaunchKernelGGL((transfer_bf16_tiled_kernel<4, false>), grid, dim3(512), 0, s, a);
+        else if (tiled)
+          hipLaunchKernelGGL((transfer_bf16_tiled_kernel<4, false>), pgrid, dim3(512), 0, s, a);
         else hipLaunchKernelGGL(transfer_bf16_direct_kernel<8>, grid, dim3(512), 0, s, a);
         break;
       default: return hipErrorInvalidValue;

@@ -152,9 +152,9 @@ def test_transfer_host_validation(L):
     assert call(sd=_desc(dtype=0, d=96), rd=_desc(L_=6, dtype=0, d=96),
                 opts=hf.hf_transfer_opts(None, C.c_void_p(0x1000), 1e-6)) == -8   # fp32 norm d_h
     # cos/sin tables: 64 sender + 60 receiver positions x 64 pairs x 8 bytes, then
-    # one 8 KB staging record per 64-row receiver tile
+    # one 8 KB staging record per 64-row receiver tile and 256 bytes of work counter
     assert L.hf_transfer_workspace_bytes(1, _p(s_len), _p(r_len), C.byref(_desc()),
-                                         C.byref(_desc(L_=6)), C.byref(r)) == 64 * 512 + 60 * 512 + 8192
+                                         C.byref(_desc(L_=6)), C.byref(r)) == 64 * 512 + 60 * 512 + 8192 + 256
 
 
 def test_transfer_workspace_records(L):
@@ -166,13 +166,14 @@ def test_transfer_workspace_records(L):
     def wsb(sd, rd):
         return L.hf_transfer_workspace_bytes(3, _p(s_len), _p(r_len), C.byref(sd), C.byref(rd), None)
 
-    # bf16 with 8 or 4 receiver heads: one record per non-empty 64-row tile
-    assert wsb(_desc(), _desc(L_=6)) == 2 * 8192
-    assert wsb(_desc(H=4), _desc(L_=6, H=4)) == 2 * 8192
+    # bf16 with 8 or 4 receiver heads: one record per non-empty 64-row tile, and
+    # the work counter
+    assert wsb(_desc(), _desc(L_=6)) == 2 * 8192 + 256
+    assert wsb(_desc(H=4), _desc(L_=6, H=4)) == 2 * 8192 + 256
     r130 = np.array([130], np.int32)
     assert L.hf_transfer_workspace_bytes(1, _p(np.array([200], np.int32)), _p(r130),
                                          C.byref(_desc(T=256)), C.byref(_desc(L_=6, T=256)),
-                                         None) == 3 * 8192
+                                         None) == 3 * 8192 + 256
     # kernels that keep no records: 2 receiver heads, more than 8 sender heads, fp32
     assert wsb(_desc(), _desc(L_=6, H=2)) == 0
     assert wsb(_desc(H=16), _desc(L_=6)) == 0
