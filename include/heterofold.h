@@ -273,8 +273,8 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  * result once to bf16.
  * Supported by this library: d_h == 128 for HF_BF16 with receiver H in
  * {2, 4, 8} and one (layer, role) map under 2 GiB; any even d_h and H for
- * HF_F32 (d_in <= 4096).  Other valid
- * shapes return HF_ERR_UNSUPPORTED.  Receiver rows past r_len are not written.
+ * HF_F32 (d_in <= 4096).  Other valid shapes return HF_ERR_UNSUPPORTED.
+ * Receiver rows past r_len are not written.
  */
 int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
                        const int32_t* row_ptr, const int32_t* col, const int32_t* num,
