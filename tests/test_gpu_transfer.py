@@ -189,6 +189,34 @@ def test_bf16_tiles_beyond_staging_capacity(torch, H_r):
 
 
 @pytest.mark.parametrize("H_r", [8, 4])
+def test_bf16_full_batch_of_short_sequences(torch, H_r):
+    # 64 sequences (the batch limit) of 0 to 200 sender tokens: many tiles with
+    # ragged tails, sequences without tiles, and fewer work items than compute
+    # units at L_r = 1, so the work decoding and the per-sequence tile starts are
+    # exercised together.
+    cfg = synth.LLAMA8B_14B_8K.with_(name=f"64 short sequences H_r={H_r}", H_r=H_r, L_r=1)
+    rng = np.random.default_rng(14)
+    parts = []
+    for n_s in rng.integers(0, 201, 64):
+        sb, se = synth.segment_tokens(rng, int(n_s), 1, 7)
+        rb, re_ = synth.segment_chars(rng, int(se[-1]) if n_s else 0, 1, 8)
+        parts.append((sb, se, rb, re_))
+    seg = synth.concat_segmentations(parts)
+    S = synth.make_cache(cfg, seg, seed=14, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=14, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=rng.integers(0, 50, 64).astype(np.int32),
+                             pos0_r=rng.integers(0, 50, 64).astype(np.int32))
+    wl = synth.Workload(cfg, seg, S, A, bias, rope)
+    T_cap = int(seg.r_len.max()) + 5
+    R = torch.full((64, cfg.L_r, 2, cfg.H_r, T_cap, cfg.d_h), 3.0, dtype=torch.bfloat16,
+                   device="cuda")
+    _compare_full(torch, cfg, wl, "overlap", R=R)
+    for b in range(64):
+        T_r = int(seg.r_len[b])
+        assert bool((R[b, :, :, :, T_r:, :] == 3.0).all()), f"sequence {b}: rows past {T_r} changed"
+
+
+@pytest.mark.parametrize("H_r", [8, 4])
 def test_bf16_runs_too_wide_for_the_rotation_table(torch, H_r):
     # One-character sender tokens under 4-6 character receiver tokens: about 5
     # entries per row, so a tile stays within the staged entry count, but a run
