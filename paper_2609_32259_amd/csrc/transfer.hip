@@ -15,6 +15,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 // ---------------------------------------------------------------------------
@@ -891,8 +892,11 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
       const int ci = lane % LPR;
       const uint4 v = *reinterpret_cast<const uint4*>(stage + rr * kXS + 8 * ci);
       const int jj = j0 + 32 * mt + rr;
-      if (jj < Tr)
-        *reinterpret_cast<uint4*>(dst_head + (long long)jj * p.r_st + feat[ci / 4] + 8 * (ci % 4)) = v;
+      if (jj < Tr)  // streaming store: the receiver rows are not read again here, so
+                    // they should not push the shared map out of L2
+        __builtin_nontemporal_store(
+            u32x4{v.x, v.y, v.z, v.w},
+            reinterpret_cast<u32x4*>(dst_head + (long long)jj * p.r_st + feat[ci / 4] + 8 * (ci % 4)));
     }
   }
   if (!kPersist || next >= n_items) break;
