@@ -217,6 +217,31 @@ def test_bf16_full_batch_of_short_sequences(torch, H_r):
 
 
 @pytest.mark.parametrize("H_r", [8, 4])
+def test_bf16_sender_slab_beyond_32_bit_offsets(torch, H_r):
+    # A sender cache with a token capacity of 1.2M: one (layer, role) slab spans
+    # 7 head strides of 1.2M x 128 bf16 (2.4 GB), past what a 32-bit buffer
+    # offset reaches, so the build reads the rows with 64-bit addresses instead.
+    cfg = synth.LLAMA8B_14B_8K.with_(name=f"1.2M-token sender capacity H_r={H_r}", H_r=H_r,
+                                     L_s=2, L_r=3)
+    rng = np.random.default_rng(15)
+    sb, se = synth.segment_tokens(rng, 300, 1, 7)
+    rb, re_ = synth.segment_chars(rng, int(se[-1]), 1, 8)
+    seg = synth.concat_segmentations([(sb, se, rb, re_)])
+    S_small = synth.make_cache(cfg, seg, seed=15, device="cuda")
+    T_cap = 1_200_000
+    assert (cfg.H_s - 1) * T_cap * cfg.d_h * 2 >= 1 << 31
+    S = torch.zeros((1, cfg.L_s, 2, cfg.H_s, T_cap, cfg.d_h), dtype=torch.bfloat16, device="cuda")
+    S[:, :, :, :, :300, :] = S_small
+    del S_small
+    A, bias = synth.make_maps(cfg, seed=15, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=np.array([7], np.int32), pos0_r=np.array([3], np.int32))
+    wl = synth.Workload(cfg, seg, S, A, bias, rope)
+    _compare_full(torch, cfg, wl, "overlap")
+    del wl, S
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("H_r", [8, 4])
 def test_bf16_runs_too_wide_for_the_rotation_table(torch, H_r):
     # One-character sender tokens under 4-6 character receiver tokens: about 5
     # entries per row, so a tile stays within the staged entry count, but a run
