@@ -133,10 +133,38 @@ def build_alignment_batched(s_cu, r_cu, s_beg, s_end, r_beg, r_end,
     return cat(rp_all), cat(col_all), cat(num_all), cat(den_all)
 
 
-def position_mismatch(s_end, r_end, a) -> float:
-    """Mean |e^S_a(j) - e^R_j| in characters over the given receiver rows
-    (App. B.1, token-position mismatch m_d).  Diagnostic only."""
-    s_end, r_end, a = map(_as_int, (s_end, r_end, a))
-    if r_end.size == 0:
+def same_index_alignment(s_beg, s_end, r_beg, r_end) -> np.ndarray:
+    """Same-index pairing, the baseline the token-position mismatch of App. B.1
+    is compared against: counting nonempty tokens from one, the k-th nonempty
+    receiver token takes the min(k, n_S)-th nonempty sender token, so receiver
+    positions past the sender sequence reuse its last token.  Returned as
+    0-based indices into the full sender token list (int64 [T_r]); an empty
+    receiver token takes the entry of the nonempty token before it (or the
+    first one), which the mismatch never reads.  With no nonempty sender
+    token every entry is 0."""
+    s_beg, s_end, r_beg, r_end = map(_as_int, (s_beg, s_end, r_beg, r_end))
+    s_ne = np.nonzero(s_beg < s_end)[0]
+    a = np.zeros(r_end.size, dtype=np.int64)
+    if s_ne.size == 0:
+        return a
+    k = 0  # nonempty receiver tokens seen so far
+    cur = int(s_ne[0])
+    for j in range(r_end.size):
+        if r_beg[j] < r_end[j]:
+            k += 1
+            cur = int(s_ne[min(k, s_ne.size) - 1])
+        a[j] = cur
+    return a
+
+
+def position_mismatch(s_beg, s_end, r_beg, r_end, a) -> float:
+    """Token-position mismatch m_d of App. B.1, in characters: the mean over
+    the nonempty receiver tokens j of |e^S_a(j) - e^R_j|, where e are the
+    character end offsets and a(j) the sender index assigned to receiver token
+    j (ta_alignment or same_index_alignment).  0 when no receiver token is
+    nonempty.  A diagnostic of the alignment; the transfer never uses it."""
+    s_beg, s_end, r_beg, r_end, a = map(_as_int, (s_beg, s_end, r_beg, r_end, a))
+    J = np.nonzero(r_beg < r_end)[0]
+    if J.size == 0:
         return 0.0
-    return float(np.mean(np.abs(s_end[a] - r_end)))
+    return float(np.mean(np.abs(s_end[a[J]] - r_end[J])))

@@ -207,3 +207,64 @@ def test_batched_matches_per_sequence():
             assert np.array_equal(col[rp[r0]:rp[r1]], pcol)
             assert np.array_equal(num[rp[r0]:rp[r1]], pnum)
             assert np.array_equal(den[r0:r1], pden)
+
+
+# --- token-position mismatch (App. B.1) ---------------------------------------
+# Hand-worked on the Sec. 3.1 example.  Qwen3 ends {3, 16, 23, 24}, Ministral-3
+# ends {3, 9, 12, 16, 23, 24}.
+#   Qwen3 -> Ministral-3, TA a = [0, 0, 0, 1, 2, 3]: sender ends [3, 3, 3, 16, 23, 24]
+#     against [3, 9, 12, 16, 23, 24] -> |diffs| [0, 6, 9, 0, 0, 0] -> 15 / 6 = 2.5.
+#   Same-index a = [0, 1, 2, 3, 3, 3]: ends [3, 16, 23, 24, 24, 24] -> [0, 7, 11, 8, 1, 0]
+#     -> 27 / 6 = 4.5.
+#   Ministral-3 -> Qwen3, TA a = [0, 3, 4, 5]: ends [3, 16, 23, 24] -> 0.
+#   Same-index a = [0, 1, 2, 3]: ends [3, 9, 12, 16] against [3, 16, 23, 24] -> 26 / 4 = 6.5.
+@pytest.mark.parametrize("src,dst,ta_m,same_a,same_m", [
+    ("qwen3", "ministral3", 2.5, [0, 1, 2, 3, 3, 3], 4.5),
+    ("ministral3", "qwen3", 0.0, [0, 1, 2, 3], 6.5)])
+def test_position_mismatch_worked_example(example, src, dst, ta_m, same_a, same_m):
+    sb, se, rb, re_ = _sides(example, src, dst)
+    a_ta = al.ta_alignment(sb, se, rb, re_)
+    assert al.position_mismatch(sb, se, rb, re_, a_ta) == ta_m
+    a_si = al.same_index_alignment(sb, se, rb, re_)
+    assert a_si.tolist() == same_a
+    assert al.position_mismatch(sb, se, rb, re_, a_si) == same_m
+
+
+def test_position_mismatch_skips_empty_receiver_tokens(example):
+    # An empty receiver token inserted at character 9 is not in J_d: the mean is
+    # still over the six nonempty tokens, and same-index counting skips it.
+    sb, se, rb, re_ = _sides(example, "qwen3", "ministral3")
+    rb2 = np.insert(rb, 2, 9)
+    re2 = np.insert(re_, 2, 9)
+    a_ta = al.ta_alignment(sb, se, rb2, re2)
+    assert al.position_mismatch(sb, se, rb2, re2, a_ta) == 2.5
+    a_si = al.same_index_alignment(sb, se, rb2, re2)
+    assert a_si.tolist() == [0, 1, 1, 2, 3, 3, 3]
+    assert al.position_mismatch(sb, se, rb2, re2, a_si) == 4.5
+
+
+def test_position_mismatch_identical_tokenizations_is_zero():
+    rng = np.random.default_rng(3)
+    sb, se = synth.segment_tokens(rng, 200, 1, 7)
+    for a in (al.ta_alignment(sb, se, sb, se), al.same_index_alignment(sb, se, sb, se)):
+        assert a.tolist() == list(range(200))
+        assert al.position_mismatch(sb, se, sb, se, a) == 0.0
+
+
+def test_position_mismatch_brute_force():
+    # Against a direct loop over nonempty receiver tokens with 1-based counting.
+    rng = np.random.default_rng(4)
+    for _ in range(20):
+        n = 300
+        sb, se = synth.segment_messy(rng, n, 1, 6)
+        rb, re_ = synth.segment_chars(rng, n, 1, 8)
+        s_ne = [i for i in range(len(sb)) if sb[i] < se[i]]
+        tot, cnt, k = 0, 0, 0
+        for j in range(len(rb)):
+            if rb[j] < re_[j]:
+                k += 1
+                i = s_ne[min(k, len(s_ne)) - 1] if s_ne else 0
+                tot += abs(int(se[i]) - int(re_[j]))
+                cnt += 1
+        a = al.same_index_alignment(sb, se, rb, re_)
+        assert al.position_mismatch(sb, se, rb, re_, a) == (tot / cnt if cnt else 0.0)
