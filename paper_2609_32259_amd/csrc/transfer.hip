@@ -575,9 +575,12 @@ __global__ __launch_bounds__(512) void stage_tiles_kernel(const TransferArgs p, 
   __syncthreads();
   const int NG = 8 * WPH;  // lane groups over the tile's rows
   if (wave == 0) {
-    if (lane <= NG) {
-      int bnd = lane == NG ? 64 : 0;
-      if (lane > 0 && lane < NG) {
+    // Boundaries gstart[0..NG]; with one sender head NG = 64, one more than the
+    // wave has lanes, so lane 0 also writes the closing boundary gstart[NG].
+    if (lane == 0) gstart[NG] = 64;
+    if (lane < NG) {
+      int bnd = 0;
+      if (lane > 0) {
         const int target = (lane * nnz + NG / 2) / NG;
         int lo = 0, hi = nrows;  // smallest r with estart[r] - e_base >= target
         while (lo < hi) {
