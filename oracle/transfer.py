@@ -81,6 +81,40 @@ def features(S, layer_table, csr, rope, layer, role):
     return _weights_matrix(csr, T_s) @ u
 
 
+def map_features(x, A_lc, b_lc, role, d_h, layer=0, rope=None, opts=None, rows=None):
+    """Steps 4-6 for one receiver layer and role, from the features the map
+    sees (x_j / r, i.e. 1/r already applied): y_j = A_lc x_j + b_lc (Eq. 9 in
+    column form), reshaped into receiver heads; keys then take the receiver's
+    key normalization (weights k_norm[layer]) and its rotation at
+    q_j = pos0_r + j.
+    x     fp64 [n, d_in]; rows: the receiver indices j of x's rows (default
+          0..n-1), used only for the rotation
+    returns fp64 [H_R, n, d_h]"""
+    _, k_norm, eps = _opts(opts)
+    x = np.asarray(x, dtype=np.float64)
+    A_lc = np.asarray(A_lc, dtype=np.float64)
+    n = x.shape[0]
+    H_r = A_lc.shape[0] // d_h
+    y = x @ A_lc.T
+    if b_lc is not None:
+        y = y + np.asarray(b_lc, dtype=np.float64)[None, :]
+    y = y.reshape(n, H_r, d_h).transpose(1, 0, 2)                           # [H_r, n, d_h]
+    if role == K and k_norm is not None:
+        y = rms_norm(y, np.asarray(k_norm)[layer], eps)
+    if role == K and rope is not None and rope.get("rotate_receiver_k", False):
+        j = np.arange(n) if rows is None else np.asarray(rows, dtype=np.int64)
+        y = _rope.rotate(y, rope.get("pos0_r", 0) + j, rope["theta_r"])
+    return y
+
+
+def scaled_features(x, layer, role, opts=None):
+    """x_j / r: the features scaled by the 1/r of Eq. 3 when opts gives it."""
+    inv_r, _, _ = _opts(opts)
+    if inv_r is None:
+        return np.asarray(x, dtype=np.float64)
+    return np.asarray(x, dtype=np.float64) * float(np.asarray(inv_r, np.float64)[layer, role])
+
+
 def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None, opts=None):
     """Whole receiver cache of one sequence.
 
@@ -93,7 +127,6 @@ def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None, opts=None):
     opts        None or dict(inv_r, k_norm, k_norm_eps) (module docstring)
     returns     [L_R, 2, H_R, T_R, d_h] fp64
     """
-    inv_r, k_norm, eps = _opts(opts)
     S = np.asarray(S, dtype=np.float64)
     A = np.asarray(A, dtype=np.float64)
     L_s, _, H_s, T_s, d_h = S.shape
@@ -106,17 +139,9 @@ def transfer(S, layer_table, csr, A, b=None, rope=None, H_r=None, opts=None):
     for l in range(L_r):
         for c in (K, V):
             x = features(S, layer_table, csr, rope, l, c)                  # [T_r, d_S]
-            if inv_r is not None:
-                x = x * float(np.asarray(inv_r, np.float64)[l, c])
-            y = x @ A[l, c].T
-            if b is not None:
-                y = y + np.asarray(b, dtype=np.float64)[l, c][None, :]
-            y = y.reshape(T_r, H_r, d_h).transpose(1, 0, 2)                 # [H_r,T_r,d_h]
-            if c == K and k_norm is not None:
-                y = rms_norm(y, np.asarray(k_norm)[l], eps)
-            if c == K and rope is not None and rope.get("rotate_receiver_k", False):
-                y = _rope.rotate(y, rope.get("pos0_r", 0) + np.arange(T_r), rope["theta_r"])
-            out[l, c] = y
+            x = scaled_features(x, l, c, opts)
+            out[l, c] = map_features(x, A[l, c], None if b is None else np.asarray(b)[l, c],
+                                     c, d_h, l, rope, opts)
     return out
 
 
@@ -209,7 +234,6 @@ def transfer_taps(S, taps, csr, A, b=None, rope=None, H_r=None, opts=None):
     A     [L_R, 2, d_R, n * d_S];  b  [L_R, 2, d_R] or None
     other arguments and the result as in ``transfer``
     """
-    inv_r, k_norm, eps = _opts(opts)
     S = np.asarray(S, dtype=np.float64)
     A = np.asarray(A, dtype=np.float64)
     taps = np.asarray(taps)
@@ -222,18 +246,9 @@ def transfer_taps(S, taps, csr, A, b=None, rope=None, H_r=None, opts=None):
     out = np.empty((L_r, 2, H_r, T_r, d_h), dtype=np.float64)
     for l in range(L_r):
         for c in (K, V):
-            x = features_taps(S, taps, csr, rope, l, c)
-            if inv_r is not None:
-                x = x * float(np.asarray(inv_r, np.float64)[l, c])
-            y = x @ A[l, c].T
-            if b is not None:
-                y = y + np.asarray(b, dtype=np.float64)[l, c][None, :]
-            y = y.reshape(T_r, H_r, d_h).transpose(1, 0, 2)
-            if c == K and k_norm is not None:
-                y = rms_norm(y, np.asarray(k_norm)[l], eps)
-            if c == K and rope is not None and rope.get("rotate_receiver_k", False):
-                y = _rope.rotate(y, rope.get("pos0_r", 0) + np.arange(T_r), rope["theta_r"])
-            out[l, c] = y
+            x = scaled_features(features_taps(S, taps, csr, rope, l, c), l, c, opts)
+            out[l, c] = map_features(x, A[l, c], None if b is None else np.asarray(b)[l, c],
+                                     c, d_h, l, rope, opts)
     return out
 
 

@@ -1,0 +1,145 @@
+"""GPU-vs-oracle comparison shared by the GPU parity tests.
+
+For one sequence of a batch, a window of receiver rows [r0, r1) (the whole
+sequence by default) and a set of receiver layers, the oracle's features are
+formed from the sender tokens the window reads (oracle.transfer.features /
+features_taps on the sliced sender cache, with the sender RoPE positions
+shifted to match), then mapped (oracle.transfer.map_features), and every
+element of the GPU result in the window is checked by _parity.check_layer.
+Windows keep full-size checks affordable: the oracle's cost grows with the
+window, not with the sequence.
+"""
+
+import numpy as np
+
+from _parity import Worst, check_layer, kernel_gate
+from oracle import alignment as al
+from oracle import layer_map as lm
+from oracle import transfer as tr
+
+
+def np64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def opts64(opts):
+    if opts is None:
+        return None
+    return dict(inv_r=np64(opts["inv_r"]), k_norm=np64(opts["k_norm"]),
+                k_norm_eps=opts["k_norm_eps"])
+
+
+def seq_rope(rope, b):
+    if rope is None:
+        return None
+    rp = dict(rope)
+    for k in ("pos0_s", "pos0_r"):
+        rp[k] = 0 if rope.get(k) is None else int(np.asarray(rope[k])[b])
+    return rp
+
+
+def csr_window(csr, r0, r1):
+    """Rows [r0, r1) of a CSR table, with sender columns shifted to start at
+    the smallest one they read: (csr_w, c0, c1) with columns in [c0, c1)."""
+    row_ptr, col, num, den = (np.asarray(t, dtype=np.int64) for t in csr)
+    e0, e1 = int(row_ptr[r0]), int(row_ptr[r1])
+    c0, c1 = int(col[e0:e1].min()), int(col[e0:e1].max()) + 1
+    return (row_ptr[r0:r1 + 1] - e0, col[e0:e1] - c0, num[e0:e1], den[r0:r1]), c0, c1
+
+
+def windows(T_r, tile, rng, n_mid=2, width=256):
+    """Receiver-row windows for a sampled check: the head, the tail, and
+    n_mid windows starting just before a row-tile edge at random."""
+    out = [(0, min(width, T_r))]
+    for _ in range(n_mid):
+        if T_r > 2 * width + tile:
+            t = int(rng.integers(1, (T_r - width) // tile)) * tile
+            out.append((t - 3, min(T_r, t - 3 + width)))
+    out.append((max(0, T_r - width), T_r))
+    return out
+
+
+class Case:
+    """One GPU result to check: cfg, workload, the receiver cache R the path
+    wrote, the alignment mode and the layer map ("interp2", "neighbor3" or an
+    explicit [L_r][n] tap table)."""
+
+    def __init__(self, cfg, wl, R, mode="overlap", layer_map=None, tag="gpu"):
+        self.cfg, self.wl, self.R, self.mode, self.tag = cfg, wl, R, mode, tag
+        lmap = cfg.layer_map if layer_map is None else layer_map
+        if isinstance(lmap, str) and lmap == "interp2":
+            self.lt, self.taps = lm.interp2(cfg.L_s, cfg.L_r), None
+        elif isinstance(lmap, str):
+            self.lt, self.taps = None, lm.neighbor3(cfg.L_s, cfg.L_r)
+        else:
+            self.lt, self.taps = None, np.asarray(lmap)
+        self.opts = opts64(wl.opts)
+        self._csr = {}
+
+    def csr(self, b):
+        if b not in self._csr:
+            self._csr[b] = al.build_alignment(*self.wl.seg.seq(b), self.mode)
+        return self._csr[b]
+
+    def qlimited(self, c):
+        """Keys with log-normal outlier channels, or after the key norm."""
+        cfg = self.cfg
+        return c == 0 and cfg.dtype == "bf16" and (bool(cfg.k_scale_sigma) or
+                                                   self.opts is not None)
+
+    def check(self, b, layers, r0=0, r1=None, roles=(0, 1), worst=None, verbose=False):
+        cfg, wl = self.cfg, self.wl
+        T_r = int(wl.seg.r_len[b])
+        r1 = T_r if r1 is None else r1
+        worst = Worst() if worst is None else worst
+        if T_r == 0 or r1 <= r0:
+            return worst
+        csr_w, c0, c1 = csr_window(self.csr(b), r0, r1)
+        rope = seq_rope(wl.rope, b)
+        rope_w = None if rope is None else dict(rope, pos0_s=rope["pos0_s"] + c0)
+        rows = np.arange(r0, r1)
+        A_all, b_all = wl.A, wl.bias
+        for l in layers:
+            if self.taps is None:
+                lo, hi, rem, den = (int(t[l]) for t in self.lt)
+                need = [lo] if rem == 0 else [lo, hi]
+                sub = (np.array([0]), np.array([len(need) - 1]), np.array([rem]), np.array([den]))
+            else:
+                need = sorted(set(int(t) for t in self.taps[l]))
+                sub = np.array([[need.index(int(t)) for t in self.taps[l]]])
+            S = np64(wl.S[b, need][:, :, :, c0:c1, :])
+            for c in roles:
+                if self.taps is None:
+                    x = tr.features(S, sub, csr_w, rope_w, 0, c)
+                else:
+                    x = tr.features_taps(S, sub, csr_w, rope_w, 0, c)
+                xs = tr.scaled_features(x, l, c, self.opts)
+                A = np64(A_all[l, c])
+                bias = None if b_all is None else np64(b_all[l, c])
+                ref = tr.map_features(xs, A, bias, c, cfg.d_h, l, rope, self.opts, rows)
+                got = np64(self.R[b, l, c, :, r0:r1, :])
+                where = f"{cfg.name} b={b} l={l} c={c} rows=[{r0},{r1})"
+                gate = None
+                if cfg.dtype == "bf16":
+                    gate = kernel_gate(xs, A, bias, c, cfg.d_h, l, rope, self.opts, rows)
+                s = check_layer(got, ref, where, dtype=cfg.dtype,
+                                max_abs="report" if self.qlimited(c) else "ulp", gate=gate)
+                worst.add(s)
+                if verbose:
+                    print(f"[{self.tag}] {where}: rel-Fro {s['rel']:.3e} max|err| {s['max']:.3e} "
+                          f"#>2e-2 {s['n_over']} #>2e-2+ulp {s['n_over_ulp']} "
+                          f"gate {s['gate']:.2f}", flush=True)
+        return worst
+
+    def check_all(self, layers=None, windows_of=None, verbose=False):
+        """Every sequence of the batch, all layers by default, whole
+        sequences or the windows windows_of(b, T_r) gives."""
+        worst = Worst()
+        layers = range(self.cfg.L_r) if layers is None else layers
+        for b in range(self.wl.seg.batch):
+            T_r = int(self.wl.seg.r_len[b])
+            spans = [(0, T_r)] if windows_of is None else windows_of(b, T_r)
+            for r0, r1 in spans:
+                self.check(b, layers, r0, r1, worst=worst, verbose=verbose)
+        print(f"[{self.tag}] {self.cfg.name}: {worst}", flush=True)
+        return worst

@@ -1,35 +1,125 @@
 """Tolerance checks shared by the GPU parity tests.
 
-bf16 outputs: per (layer, role), relative Frobenius error <= 5e-3 and max
-elementwise |error| <= 2e-2 against the fp64 oracle.
+bf16 outputs are checked per (layer, role) against the fp64 oracle three ways:
 
-One workload draws log-normal(0, 1) per-channel key scales, so a few feature
-channels reach |x| ~ 1e2.  There the bf16 representation itself forbids the
-literal max-abs gate: the mapped features are bf16 (half-ulp 0.5 at
-|x| in [128, 256)) and so are the outputs (half-ulp 1/32 at |y| in [8, 16)).
-For that case ("quantization-limited") every element must satisfy
-|error| <= 2e-2, or else lie within the worst-case first-order error of the
-two roundings the arithmetic performs,
-    half_ulp(y) + sum_k |A_nk| half_ulp(x_k)   (+ an fp32 accumulation term),
-which a wrong index, sign or dropped term would exceed.
-Keys that go through the receiver's key normalization (RMSNorm per head,
-then RoPE) have |y| of several units, where the output's own half-ulp
-(1/64 at |y| in [4, 8)) again leaves little room under 2e-2.  They are
-gated the same way with the first-order bound carried through the norm and
-the rotation (``rounding_bound_normed``).
-fp32 outputs: the same gates, plus relative Frobenius error <= 1e-5.
+1. Relative Frobenius error <= 5e-3 (literal, everywhere).
+2. Max elementwise |error| <= 2e-2.  Read as SURVEY's R13 asks: the output is
+   bf16, and its own rounding (half-ulp 1/64 at |y| in [4, 8), 1/32 in
+   [8, 16)) can carry an otherwise exact result past 2e-2.  So no element may
+   exceed 2e-2 + ulp(y), and the count of elements above 2e-2 is reported
+   ("quantization-limited"; max_abs="ulp").  The literal bound is asserted
+   where a test asks for it (max_abs="literal").  For keys with
+   log-normal(0, 1) outlier channels, and keys after the receiver's key
+   normalization, the features themselves are quantization-limited (a
+   feature |x| in [128, 256) is stored with a half-ulp of 0.5), so only the
+   counts are reported there (max_abs="report") and gate 3 decides.
+3. The kernel-arithmetic gate, for every bf16 role.  The path rounds the
+   features x_j once to bf16 (round to nearest even), multiplies and
+   accumulates in fp32, runs the epilogue in fp32 and rounds the output once
+   to bf16.  The reference for that arithmetic is the oracle's own map
+   (``oracle.transfer.map_features``) applied to bf16(x_j), with x_j the
+   oracle's fp64 features: ref_q.  Each output must lie within
+       E + half_ulp(|ref_q| + E)
+   of ref_q, where E bounds what fp32 arithmetic can add:
+     * where an fp64 feature sits within 2^-16 (relative) of a bf16 rounding
+       midpoint, the kernel's fp32 feature may round the other way; that
+       feature then moves by one ulp: sum over such k of |A_nk| ulp(x_k);
+     * fp32 accumulation of K products: K 2^-24 sum_k |A_nk| |bf16(x_k)|;
+     * bias, key norm and rotation in fp32: 2^-20 of the magnitudes;
+   carried through the key norm (rms rho: g (e / rho + |y| |e|_2 /
+   (sqrt(d_h) rho^2))) and through RoPE's pair mixing.  E is typically
+   1e-4..1e-3, so the gate is about half an output ulp: far tighter than
+   2e-2, and independent of the quantization-limited reading.
+
+fp32 outputs: gates 1 and 2, plus relative Frobenius error <= 1e-5.
 """
 
 import numpy as np
+
+from oracle import transfer as _tr
 
 REL_FRO = 5e-3
 MAX_ABS = 2e-2
 
 
+def _t(a):
+    """A float64 torch CPU view of a (elementwise work on the CPU's threads)."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(np.asarray(a, dtype=np.float64)))
+
+
+def _exponent_t(t):
+    """floor(log2|t|) of the fp32 value of t (at least -126), as float64."""
+    import torch
+    e = (t.abs().float().view(torch.int32) >> 23) - 127
+    return e.clamp_(min=-126).double()
+
+
 def bf16_half_ulp(y):
-    a = np.abs(np.asarray(y, dtype=np.float64))
-    e = np.floor(np.log2(np.maximum(a, 2.0 ** -126)))
-    return 2.0 ** (e - 8)
+    import torch
+    return torch.exp2(_exponent_t(_t(y)) - 8).numpy()
+
+
+def bf16_ulp(y):
+    return 2.0 * bf16_half_ulp(y)
+
+
+def bf16_round(x):
+    """fp64 -> fp32 -> bf16, round to nearest even (as the path rounds its
+    fp32 features), returned as fp64."""
+    import torch
+    return _t(x).float().to(torch.bfloat16).double().numpy()
+
+
+def near_midpoint(x):
+    """Features whose value lies within 2^-16 (relative, at most) of a bf16
+    rounding midpoint, where an fp32 value of the same sum may round either
+    way: the low 16 bits of the fp32 mantissa within 128 fp32 ulps of 0x8000."""
+    import torch
+    u = _t(x).float().view(torch.int32)
+    return (((u & 0xFFFF) - 0x8000).abs() <= 128).logical_and_((u & 0x7FFFFFFF) != 0).numpy()
+
+
+def kernel_gate(xs, A_lc, b_lc, role, d_h, layer=0, rope=None, opts=None, rows=None):
+    """ref_q and the per-element bound of gate 3 for one (layer, role).
+    xs [n, K] the oracle's fp64 features as the map sees them (1/r applied);
+    A_lc [d_R, K]; b_lc [d_R] or None; rows the receiver indices of xs's rows.
+    Returns (ref_q, bound), each [H_R, n, d_h].  The accumulation term uses
+    sum_k |A_nk| |x_k| <= |A_n|_2 |x|_2."""
+    import scipy.sparse as sp
+    import torch
+    xs = np.asarray(xs, dtype=np.float64)
+    A = np.asarray(A_lc, dtype=np.float64)
+    n, K = xs.shape
+    H_r = A.shape[0] // d_h
+    xq = bf16_round(xs)
+    ref_q = _tr.map_features(xq, A, b_lc, role, d_h, layer, rope, opts, rows)
+    r, c = np.nonzero(near_midpoint(xs))
+    flip = sp.csr_matrix((bf16_ulp(xs[r, c]), (r, c)), shape=(n, K)) @ np.abs(A).T
+    e = _t(flip)
+    e += K * 2.0 ** -24 * torch.outer(_t(np.linalg.norm(xq, axis=1)), _t(np.linalg.norm(A, axis=1)))
+    y = _t(xq @ A.T)
+    if b_lc is not None:
+        bb = _t(b_lc)[None, :]
+        y += bb
+        e += 2.0 ** -20 * (y.abs() + bb.abs())
+    else:
+        e += 2.0 ** -20 * y.abs()
+    e = e.reshape(n, H_r, d_h).transpose(0, 1)
+    y = y.reshape(n, H_r, d_h).transpose(0, 1)
+    rq = _t(ref_q)
+    _, k_norm, eps = _tr._opts(opts)
+    if role == _tr.K and k_norm is not None:
+        g = _t(k_norm)[layer].abs()
+        rho = ((y * y).mean(dim=-1, keepdim=True) + eps).sqrt()
+        en = torch.linalg.vector_norm(e, dim=-1, keepdim=True)
+        e = g * (e / rho + y.abs() * en / (np.sqrt(d_h) * rho * rho)) + 2.0 ** -20 * g * y.abs() / rho
+    if role == _tr.K and rope is not None and rope.get("rotate_receiver_k", False):
+        h = d_h // 2
+        mix = e[..., :h] + e[..., h:] + 2.0 ** -20 * (rq[..., :h].abs() + rq[..., h:].abs())
+        e = torch.cat([mix, mix], dim=-1)
+    bound = e + torch.exp2(_exponent_t(rq.abs() + e) - 8)
+    return ref_q, bound.numpy()
 
 
 def err_stats(got, ref):
@@ -41,57 +131,59 @@ def err_stats(got, ref):
     return rel, (float(np.max(np.abs(d))) if d.size else 0.0), d
 
 
-def rounding_bound(ref, x, A):
-    """Per-element first-order bound of bf16-rounding x and y.
-    ref [H_r, T, d_h] oracle outputs; x [T, d_S] oracle features; A [d_R, d_S]."""
-    H_r, T, d_h = ref.shape
-    Aa = np.abs(np.asarray(A, dtype=np.float64))
-    bx = bf16_half_ulp(x) @ Aa.T                         # [T, d_R]
-    acc = 1e-5 * (np.abs(x) @ Aa.T)                      # fp32 accumulation, generous
-    b = (bx + acc).reshape(T, H_r, d_h).transpose(1, 0, 2)
-    return bf16_half_ulp(np.abs(ref) * (1 + 2.0 ** -7) + b) + b
-
-
-def rounding_bound_normed(ref, x, A, b, g, eps, rotated):
-    """First-order bound for keys y = R(q) norm(A x + b) with x and y rounded
-    to bf16.  ref [H_r, T, d_h] oracle outputs; x [T, d_S] oracle features
-    (as the map sees them, 1/r applied); A [d_R, d_S]; b [d_R] or None;
-    g [d_h] norm weights; eps; rotated: whether the receiver RoPE follows."""
-    H_r, T, d_h = ref.shape
-    Aa = np.abs(np.asarray(A, dtype=np.float64))
-    x = np.asarray(x, dtype=np.float64)
-    y = x @ np.asarray(A, dtype=np.float64).T
-    if b is not None:
-        y = y + np.asarray(b, dtype=np.float64)[None, :]
-    e = bf16_half_ulp(x) @ Aa.T + 1e-5 * (np.abs(x) @ Aa.T)          # error before the norm
-    y = y.reshape(T, H_r, d_h)
-    e = e.reshape(T, H_r, d_h)
-    rho = np.sqrt(np.mean(y * y, axis=-1, keepdims=True) + float(eps))
-    en = np.linalg.norm(e, axis=-1, keepdims=True)
-    gg = np.abs(np.asarray(g, dtype=np.float64))
-    e = gg * (e / rho + np.abs(y) * en / (np.sqrt(d_h) * rho * rho))  # through the RMSNorm
-    e = e + 1e-6 * gg * np.abs(y) / rho
-    if rotated:                                                       # pair mixing by RoPE
-        h = d_h // 2
-        e = np.concatenate([e[..., :h] + e[..., h:], e[..., :h] + e[..., h:]], axis=-1)
-    e = e.transpose(1, 0, 2)
-    return bf16_half_ulp(np.abs(ref) * (1 + 2.0 ** -7) + e) + e
-
-
-def check_layer(got, ref, where, dtype="bf16", quantization_limited=False, x=None, A=None,
-                bound=None):
-    rel, mx, d = err_stats(got, ref)
-    assert np.all(np.isfinite(got)), f"{where}: non-finite output"
+def check_layer(got, ref, where, dtype="bf16", max_abs="ulp", gate=None):
+    """Gates 1-3 (module docstring) for one (layer, role).  max_abs:
+    "literal", "ulp" or "report" (gate 2); gate: the (ref_q, bound) pair of
+    ``kernel_gate``, required for bf16.  Returns a dict with rel-Fro, max
+    |err|, the two counts and the kernel-gate margin."""
+    import torch
+    g, r = _t(got), _t(ref)
+    assert bool(torch.isfinite(g).all()), f"{where}: non-finite output"
+    d = (g - r).abs()
+    nref = float(torch.linalg.vector_norm(r))
+    nd = float(torch.linalg.vector_norm(d))
+    rel = nd / nref if nref > 0 else nd
+    mx = float(d.max()) if d.numel() else 0.0
+    n_over = int((d > MAX_ABS).sum())
+    n_over_ulp = int((d > MAX_ABS + 2.0 * torch.exp2(_exponent_t(r) - 8)).sum())
+    stats = {"rel": rel, "max": mx, "n_over": n_over, "n_over_ulp": n_over_ulp, "gate": 0.0}
     assert rel <= REL_FRO, f"{where}: rel Frobenius {rel:.3e} > {REL_FRO}"
     if dtype == "f32":
         assert rel <= 1e-5, f"{where}: fp32 rel Frobenius {rel:.3e} > 1e-5"
-    if quantization_limited:
-        if bound is None:
-            assert x is not None and A is not None, "quantization-limited gate needs x and A"
-            bound = rounding_bound(ref, x, A)
-        bad = (np.abs(d) > MAX_ABS) & (np.abs(d) > bound)
-        assert not bad.any(), (f"{where}: {int(bad.sum())} elements beyond both 2e-2 and the "
-                               f"rounding bound; worst |err| {mx:.3e}")
-    else:
+    assert max_abs in ("literal", "ulp", "report"), max_abs
+    if max_abs == "literal" or dtype == "f32":
         assert mx <= MAX_ABS, f"{where}: max |err| {mx:.3e} > {MAX_ABS}"
-    return rel, mx
+    elif max_abs == "ulp":
+        assert n_over_ulp == 0, (f"{where}: {n_over_ulp} elements beyond 2e-2 + ulp(y); "
+                                 f"max |err| {mx:.3e}")
+    if dtype == "bf16":
+        assert gate is not None, f"{where}: bf16 check needs the kernel-arithmetic gate"
+        ref_q, bound = gate
+        dq = (g - _t(ref_q)).abs()
+        ratio = dq / _t(bound)
+        stats["gate"] = float(ratio.max()) if dq.numel() else 0.0
+        n_bad = int((ratio > 1.0).sum())
+        assert n_bad == 0, (f"{where}: {n_bad} elements outside the kernel-arithmetic gate; "
+                            f"worst |got - ref_q| {float(dq.max()):.3e}, "
+                            f"worst ratio {stats['gate']:.2f}")
+    return stats
+
+
+class Worst:
+    """Running worst case over the layers of a test, for its log line."""
+
+    def __init__(self):
+        self.rel = self.max = self.gate = 0.0
+        self.n_over = self.n_over_ulp = 0
+
+    def add(self, s):
+        self.rel = max(self.rel, s["rel"])
+        self.max = max(self.max, s["max"])
+        self.gate = max(self.gate, s["gate"])
+        self.n_over += s["n_over"]
+        self.n_over_ulp += s["n_over_ulp"]
+
+    def __str__(self):
+        return (f"worst rel-Fro {self.rel:.3e}, max|err| {self.max:.3e}, "
+                f"#|err|>2e-2: {self.n_over}, #|err|>2e-2+ulp(y): {self.n_over_ulp}, "
+                f"kernel-gate ratio {self.gate:.2f}")

@@ -1,18 +1,18 @@
 """GPU parity of the concatenated-tap transfer (the paper's three-layer
 neighbourhood map, Sec. 3.1 Eq. 1-2): hf_transfer_kv_taps against the fp64
-oracle ``transfer_taps``.  Small cases element by element over every layer,
-role and row; the full-size 32K workload on sampled rows in the launch
-configuration the benchmark times."""
+oracle (``features_taps`` + ``map_features``, as ``transfer_taps``).  Small
+cases element by element over every layer, role and row; the full-size 32K
+workload on every layer and role, over windows of rows (head, tail, across
+row-tile edges), in the launch configuration the benchmark times.  Gates:
+tests/_parity.py."""
 
 import numpy as np
 import pytest
 
-from oracle import alignment as al
 from oracle import layer_map as lm
-from oracle import transfer as tr
 from paper_2609_32259_amd import synth
 
-from _parity import check_layer
+from _compare import Case, windows
 
 pytestmark = pytest.mark.gpu
 
@@ -26,12 +26,7 @@ def torch():
     return torch
 
 
-def _np64(t):
-    return t.float().cpu().numpy().astype(np.float64)
-
-
 def _run(torch, cfg, wl, mode, taps, R=None):
-    from paper_2609_32259_amd import heterofold as hf
     from paper_2609_32259_amd.path import TransferPath
     path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r, mode=mode, R=R,
                         layer_map="neighbor3")
@@ -45,37 +40,12 @@ def _run(torch, cfg, wl, mode, taps, R=None):
     return path
 
 
-def _compare_full(torch, cfg, wl, mode="overlap", taps=None, qlimited_k=False):
+def _compare_full(torch, cfg, wl, mode="overlap", taps=None):
     taps_np = lm.neighbor3(cfg.L_s, cfg.L_r) if taps is None else np.asarray(taps)
     print(f"[gpu-taps] {cfg.name} mode={mode} B={wl.seg.batch} T_r={list(wl.seg.r_len)} "
           f"n_taps={taps_np.shape[1]} rope={wl.rope is not None}", flush=True)
     path = _run(torch, cfg, wl, mode, taps)
-    worst = (0.0, 0.0)
-    for b in range(wl.seg.batch):
-        T_r = int(wl.seg.r_len[b])
-        if T_r == 0:
-            continue
-        sb, se, rb, re_ = wl.seg.seq(b)
-        csr = al.build_alignment(sb, se, rb, re_, mode)
-        T_s = int(wl.seg.s_len[b])
-        S = _np64(wl.S[b, :, :, :, :T_s, :])
-        rp = None
-        if wl.rope is not None:
-            rp = dict(wl.rope)
-            for k in ("pos0_s", "pos0_r"):
-                rp[k] = 0 if wl.rope.get(k) is None else int(np.asarray(wl.rope[k])[b])
-        bias = None if wl.bias is None else _np64(wl.bias)
-        ref = tr.transfer_taps(S, taps_np, csr, _np64(wl.A), bias, rp, H_r=cfg.H_r)
-        got = _np64(path.R[b, :, :, :, :T_r, :])
-        for l in range(cfg.L_r):
-            for c in range(2):
-                ql = qlimited_k and c == 0
-                x = tr.features_taps(S, taps_np, csr, None, l, c) if ql else None
-                rel, mx = check_layer(got[l, c], ref[l, c], f"{cfg.name} b={b} l={l} c={c}",
-                                      dtype=cfg.dtype, quantization_limited=ql, x=x,
-                                      A=_np64(wl.A[l, c]) if ql else None)
-                worst = (max(worst[0], rel), max(worst[1], mx))
-    print(f"[gpu-taps]   worst rel-Fro {worst[0]:.3e}, max|err| {worst[1]:.3e}", flush=True)
+    Case(cfg, wl, path.R, mode, layer_map=taps_np, tag="gpu-taps").check_all()
 
 
 @pytest.mark.parametrize("mode", ["overlap", "ta"])
@@ -96,7 +66,7 @@ def test_taps_bf16_four_receiver_heads_outlier_keys(torch):
     cfg = synth.LLAMA8B_QWEN7B_4K.with_(name="qwen7b n3 small", layer_map="neighbor3", T_s=400,
                                         L_r=5)
     wl = synth.make_workload(cfg, seed=22, device="cuda")
-    _compare_full(torch, cfg, wl, "overlap", qlimited_k=True)
+    _compare_full(torch, cfg, wl, "overlap")
 
 
 def test_taps_bf16_two_receiver_heads(torch):
@@ -175,21 +145,12 @@ def test_taps_bf16_identity_first_block_is_bit_exact(torch):
 
 
 def test_full_14b_shape_32k_neighbor3(torch):
-    """The benchmark's neighbourhood-map workload, sampled rows."""
+    """The benchmark's neighbourhood-map workload: every layer and role, on
+    windows of rows."""
     cfg = synth.LLAMA8B_14B_32K_N3
     wl = synth.make_workload(cfg, seed=0, device="cuda")
     print(f"[gpu-taps] full-size {cfg.name} T_r={list(wl.seg.r_len)}", flush=True)
     path = _run(torch, cfg, wl, "overlap", None)
-    taps = lm.neighbor3(cfg.L_s, cfg.L_r)
-    T_r = int(wl.seg.r_len[0])
     rng = np.random.default_rng(98)
-    rows = sorted({0, 1, 63, 64, T_r // 2, T_r - 2, T_r - 1, *rng.integers(0, T_r, 20).tolist()})
-    csr = al.build_alignment(*wl.seg.seq(0), "overlap")
-    rp = dict(wl.rope, pos0_s=0, pos0_r=0)
-    get = lambda l, c, idx: _np64(wl.S[0, l, c][:, torch.as_tensor(idx, device="cuda"), :])  # noqa: E731
-    for l in (0, 2, 20, 39):
-        for c in (0, 1):
-            ref = tr.transfer_rows_taps(get, taps, csr, _np64(wl.A[l, c]), _np64(wl.bias[l, c]),
-                                        rp, cfg.d_h, l, c, rows)
-            got = _np64(path.R[0, l, c][:, torch.as_tensor(rows, device="cuda"), :])
-            check_layer(got, ref, f"{cfg.name} l={l} c={c} rows={len(rows)}")
+    Case(cfg, wl, path.R, tag="gpu-taps-32k").check_all(
+        windows_of=lambda b, T_r: windows(T_r, 64, rng, n_mid=2, width=384))
