@@ -261,6 +261,46 @@ def run_calibration(args, cfg):
     print(json.dumps(out), flush=True)
 
 
+def run_gemm_yardstick(args, cfg):
+    """A plain library GEMM of the transfer's shape, as a yardstick for what a
+    dense bf16 contraction reaches on this chip at the clock it holds: one
+    batched product of 2 L_r (layer, role) pairs, [T_r x d_in] x [d_in x d_r]
+    each, through torch.bmm (hipBLASLt), operands contiguous.  The features
+    are random: nothing of the method is computed here."""
+    import torch
+    from paper_2609_32259_amd import synth
+
+    seg = synth.make_segmentation(cfg, seed=args.seed)
+    M = int(seg.r_len.sum())
+    K, N, L = cfg.d_map_in, cfg.d_r, 2 * cfg.L_r
+    g = torch.Generator(device="cuda")
+    g.manual_seed(args.seed)
+    X = torch.randn((L, M, K), generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    W = (torch.randn((L, K, N), generator=g, device="cuda", dtype=torch.float32)
+         / K ** 0.5).to(torch.bfloat16)
+    Y = torch.empty((L, M, N), device="cuda", dtype=torch.bfloat16)
+    log(f"[yardstick] bmm bf16 {L} x [{M} x {K}] x [{K} x {N}]; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        torch.bmm(X, W, out=Y)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:
+        a.record()
+        torch.bmm(X, W, out=Y)
+        b.record()
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    flops = 2.0 * L * M * K * N
+    tf = flops / (ms.mean() * 1e-3) / 1e12
+    out = {"yardstick": "torch.bmm bf16 (hipBLASLt)", "workload": cfg.name,
+           "shape": {"batch": L, "M": M, "K": K, "N": N}, "steps": args.steps,
+           "ms_mean": round(float(ms.mean()), 4), "ms_median": round(float(np.median(ms)), 4),
+           "ms_min": round(float(ms.min()), 4), "tflops": round(tf, 1),
+           "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -269,6 +309,8 @@ def main():
     ap.add_argument("--workload", default="14b-32k")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gemm-yardstick", action="store_true",
+                    help="time a plain hipBLASLt bf16 GEMM of the workload's shape instead")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first run one plain device copy of this many MiB (a known-size "
                          "reference for hardware byte counters)")
@@ -297,6 +339,9 @@ def main():
         run_calibration(args, synth.CALIB_CONFIGS[args.workload])
         return
     cfg = synth.CONFIGS[args.workload]
+    if args.gemm_yardstick:
+        run_gemm_yardstick(args, cfg)
+        return
     log(f"[bench] workload {cfg.name}: generating inputs on the GPU")
     wl = synth.make_workload(cfg, seed=args.seed, device="cuda")
     path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r,
