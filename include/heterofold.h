@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define HF_VERSION 1
+#define HF_VERSION 2
 #define HF_MAX_BATCH 64   /* sequences per call */
 #define HF_MAX_LAYERS 128 /* receiver layers per call */
 
@@ -101,12 +101,17 @@ int32_t hf_version(void);
 /* ------------------------------------------------------------------------ */
 
 /*
- * Upper bound on the CSR entries hf_build_alignment writes for valid spans:
- * sum over sequences of (T_s + 2 T_r).  s_cu, r_cu: host [B+1] prefix sums
- * of the per-sequence sender / receiver token counts (s_cu[0] = r_cu[0] = 0).
- * Returns -1 on bad arguments.
+ * Entries the col / num buffers of hf_build_alignment must hold for valid
+ * spans of B sequences: the sum over sequences of T_s + 2 T_r in
+ * HF_ALIGN_OVERLAP mode (a receiver row reads the sender tokens its span
+ * overlaps: with both tokenizations tiling one text, the distinct boundaries
+ * of the two, at most T_s + T_r; plus one fallback entry per empty or
+ * uncovered row), and of T_r in HF_ALIGN_TA mode (one entry per row).
+ * s_len, r_len: host int32 [B] sender / receiver token counts.
+ * Returns -1 (and sets hf_last_error) on bad arguments.
  */
-int64_t hf_alignment_nnz_capacity(int32_t B, const int32_t* s_cu, const int32_t* r_cu);
+int64_t hf_alignment_nnz_capacity(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                                  int32_t mode);
 
 /* Workspace bytes hf_build_alignment needs for this batch. */
 size_t hf_alignment_workspace_bytes(int32_t B, const int32_t* r_cu);
@@ -138,8 +143,8 @@ size_t hf_alignment_workspace_bytes(int32_t B, const int32_t* r_cu);
  *   den      int32 [r_cu[B]]       weight denominator of the row.
  *   Entries of a row are in ascending col order.  For valid spans the table
  *   is unique and the result is bit-exact.
- * nnz_capacity must be >= hf_alignment_nnz_capacity(); otherwise
- * HF_ERR_CAPACITY.  (Spans that break the validity rule may need more; the
+ * nnz_capacity must be >= hf_alignment_nnz_capacity() for the same lengths
+ * and mode; otherwise HF_ERR_CAPACITY.  (Spans that break the validity rule may need more; the
  * kernels then drop entries past the capacity and clamp row_ptr to it.)
  * workspace: device, >= hf_alignment_workspace_bytes() bytes, 16-B aligned.
  */
@@ -217,7 +222,10 @@ typedef struct hf_rope {
   const int32_t* pos0_r;
 } hf_rope;
 
-/* Bytes of the packed maps for L_r receiver layers, 2 roles, d_r x d_in. */
+/* Bytes of a packed map buffer for L_r receiver layers, 2 roles, d_r x d_in:
+ * an HF_PACKED_HEADER_BYTES header (what was packed) followed by the maps in
+ * fragment order, so it is larger than the unpacked maps.  0 on bad arguments. */
+#define HF_PACKED_HEADER_BYTES 256
 size_t hf_packed_maps_bytes(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype);
 
 /*
@@ -226,8 +234,11 @@ size_t hf_packed_maps_bytes(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtyp
  * index h*d_h + e, to receiver feature n = h'*d_h + e'; this is the transpose
  * of the paper's row-vector A_final of Eq. 9, with the scalar 1/r of Eq. 3
  * already folded in).  A_packed: device, hf_packed_maps_bytes() bytes,
- * 16-B aligned, not overlapping A.  Maps are static, so this runs once per
- * model pair.  bf16 needs d_in % 16 == 0 and d_r % 32 == 0.
+ * 16-B aligned, not overlapping A; it receives a header (the word "HFPK",
+ * layout version, dtype, L_r, d_r, d_in) and the maps re-laid out in the
+ * matrix-core fragment order the bf16 kernels read (fp32 maps are copied
+ * row-major).  Maps are static, so this runs once per model pair.  bf16 needs
+ * d_in % 16 == 0 and d_r % 32 == 0.
  */
 int32_t hf_pack_maps(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype, const void* A,
                      void* A_packed, void* stream);
@@ -263,6 +274,9 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  *   sender, receiver         cache descriptors; same dtype and d_h.
  *                  receiver->L is L_r; d_in = sender->H*d_h, d_r = receiver->H*d_h.
  *   A_packed       device: maps packed by hf_pack_maps (same L_r, d_r, d_in, dtype).
+ *   A_packed_bytes the size of that buffer; anything other than
+ *                  hf_packed_maps_bytes(L_r, d_r, d_in, dtype) -- an unpacked map
+ *                  [L_r][2][d_r][d_in] in particular -- returns HF_ERR_SHAPE.
  *   bias           device fp32 [L_r][2][d_r], or NULL for zero bias.
  *   rope           NULL = no RoPE.
  *   opts           NULL, or the optional 1/r and key normalization (above).
@@ -273,16 +287,17 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  * result once to bf16.
  * Supported by this library: d_h == 128 for HF_BF16 with receiver H in
  * {2, 4, 8} and one (layer, role) map under 2 GiB; any even d_h and H for
- * HF_F32 (d_in <= 4096).  Other valid shapes return HF_ERR_UNSUPPORTED.
+ * HF_F32 (d_in <= 4096).  Other valid shapes -- bf16 with d_h == 64 among
+ * them -- return HF_ERR_UNSUPPORTED before anything is launched.
  * Receiver rows past r_len are not written.
  */
 int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
                        const int32_t* row_ptr, const int32_t* col, const int32_t* num,
                        const int32_t* den, const int32_t* lo, const int32_t* hi,
                        const int32_t* rem, const int32_t* den_l, const hf_kv_desc* sender,
-                       const hf_kv_desc* receiver, const void* A_packed, const float* bias,
-                       const hf_rope* rope, const hf_transfer_opts* opts, void* workspace,
-                       size_t workspace_bytes, void* stream);
+                       const hf_kv_desc* receiver, const void* A_packed, size_t A_packed_bytes,
+                       const float* bias, const hf_rope* rope, const hf_transfer_opts* opts,
+                       void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * hf_transfer_kv for maps over concatenated sender layers (Sec. 3.1 Eq. 2,
@@ -296,7 +311,8 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
  *   n_taps     1..3 (3 for hf_build_layer_taps's table)
  *   taps       host int32 [receiver->L][n_taps], sender layers in [0, sender->L)
  *   A_packed   maps A[l, c] of shape [d_r][n_taps * d_in] packed by
- *              hf_pack_maps with its d_in argument = n_taps * sender->H * d_h.
+ *              hf_pack_maps with its d_in argument = n_taps * sender->H * d_h;
+ *              A_packed_bytes its size, checked as in hf_transfer_kv.
  * Shapes supported, numerics, ownership and errors as hf_transfer_kv; for
  * HF_F32 the limit is n_taps * d_in <= 4096.
  */
@@ -304,8 +320,8 @@ int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_le
                             const int32_t* row_ptr, const int32_t* col, const int32_t* num,
                             const int32_t* den, int32_t n_taps, const int32_t* taps,
                             const hf_kv_desc* sender, const hf_kv_desc* receiver,
-                            const void* A_packed, const float* bias, const hf_rope* rope,
-                            const hf_transfer_opts* opts, void* workspace,
+                            const void* A_packed, size_t A_packed_bytes, const float* bias,
+                            const hf_rope* rope, const hf_transfer_opts* opts, void* workspace,
                             size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */

@@ -65,7 +65,8 @@ Profiler& prof() {
 // made while it lives, when the profiler is on.
 class TimedLaunch {
  public:
-  TimedLaunch(int kernel, hipStream_t s) : kernel_(kernel), s_(s) {
+  TimedLaunch(int kernel, hipStream_t s, bool enabled = true) : kernel_(kernel), s_(s) {
+    if (!enabled) return;
     Profiler& p = prof();
     std::lock_guard<std::mutex> g(p.mu);
     if (!p.on) return;
@@ -171,14 +172,26 @@ int32_t hf_validate_offsets_host(int32_t T, const int32_t* beg, const int32_t* e
   return ok();
 }
 
-int64_t hf_alignment_nnz_capacity(int32_t B, const int32_t* s_cu, const int32_t* r_cu) {
-  if (B < 1 || B > HF_MAX_BATCH || !s_cu || !r_cu) {
-    fail(HF_ERR_SHAPE, "need 1 <= B <= %d and non-NULL prefix sums", HF_MAX_BATCH);
+int64_t hf_alignment_nnz_capacity(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                                  int32_t mode) {
+  if (B < 1 || B > HF_MAX_BATCH || !s_len || !r_len) {
+    fail(HF_ERR_SHAPE, "need 1 <= B <= %d and non-NULL lengths", HF_MAX_BATCH);
     return -1;
   }
-  if (check_prefix("s_cu", B, s_cu) || check_prefix("r_cu", B, r_cu)) return -1;
+  if (mode != HF_ALIGN_OVERLAP && mode != HF_ALIGN_TA) {
+    fail(HF_ERR_MODE, "alignment mode %d unknown", mode);
+    return -1;
+  }
+  int64_t cap = 0;
+  for (int b = 0; b < B; ++b) {
+    if (s_len[b] < 0 || r_len[b] < 0) {
+      fail(HF_ERR_SHAPE, "negative length in sequence %d", b);
+      return -1;
+    }
+    cap += mode == HF_ALIGN_TA ? (int64_t)r_len[b] : (int64_t)s_len[b] + 2 * (int64_t)r_len[b];
+  }
   ok();
-  return (int64_t)s_cu[B] + 2 * (int64_t)r_cu[B];
+  return cap;
 }
 
 size_t hf_alignment_workspace_bytes(int32_t B, const int32_t* r_cu) {
@@ -206,8 +219,8 @@ int32_t hf_build_alignment(int32_t B, const int32_t* s_cu, const int32_t* r_cu,
   if (nR > 0 && (!r_beg || !r_end || !den)) return fail(HF_ERR_NULL, "receiver spans / den is NULL");
   if (nS > 0 && (!s_beg || !s_end)) return fail(HF_ERR_NULL, "sender spans are NULL");
   if (nR > 0 && (!col || !num)) return fail(HF_ERR_NULL, "col / num is NULL");
-  const int64_t need = nS + 2 * nR;
-  if (need > INT32_MAX) return fail(HF_ERR_SHAPE, "batch too large for int32 CSR offsets");
+  if (nS + 2 * nR > INT32_MAX) return fail(HF_ERR_SHAPE, "batch too large for int32 CSR offsets");
+  const int64_t need = mode == HF_ALIGN_TA ? nR : nS + 2 * nR;  // hf_alignment_nnz_capacity
   if (nnz_capacity < need)
     return fail(HF_ERR_CAPACITY, "nnz_capacity %lld < required %lld", (long long)nnz_capacity, (long long)need);
 
@@ -303,7 +316,8 @@ int32_t hf_build_layer_taps(int32_t L_s, int32_t L_r, int32_t* taps) {
 size_t hf_packed_maps_bytes(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype) {
   if (L_r < 1 || d_r < 1 || d_in < 1) return 0;
   const size_t el = dtype == HF_BF16 ? 2 : (dtype == HF_F32 ? 4 : 0);
-  return (size_t)L_r * 2 * (size_t)d_r * (size_t)d_in * el;
+  if (el == 0) return 0;
+  return HF_PACKED_HEADER_BYTES + (size_t)L_r * 2 * (size_t)d_r * (size_t)d_in * el;
 }
 
 int32_t hf_pack_maps(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype, const void* A,
@@ -320,7 +334,8 @@ int32_t hf_pack_maps(int32_t L_r, int32_t d_r, int32_t d_in, int32_t dtype, cons
   const size_t bytes = hf_packed_maps_bytes(L_r, d_r, d_in, dtype);
   const char* a0 = static_cast<const char*>(A);
   const char* p0 = static_cast<const char*>(A_packed);
-  if (a0 < p0 + bytes && p0 < a0 + bytes) return fail(HF_ERR_SHAPE, "A and A_packed overlap");
+  if (a0 < p0 + bytes && p0 < a0 + (bytes - HF_PACKED_HEADER_BYTES))
+    return fail(HF_ERR_SHAPE, "A and A_packed overlap");
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   {
@@ -399,9 +414,10 @@ struct LayerSpec {
 int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
                       const int32_t* row_ptr, const int32_t* col, const int32_t* num,
                       const int32_t* den, const LayerSpec& ls, const hf_kv_desc* sender,
-                      const hf_kv_desc* receiver, const void* A_packed, const float* bias,
-                      const hf_rope* rope, const hf_transfer_opts* opts, void* workspace,
-                      size_t workspace_bytes, void* stream) {
+                      const hf_kv_desc* receiver, const void* A_packed, size_t A_packed_bytes,
+                      const float* bias, const hf_rope* rope, const hf_transfer_opts* opts,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  const bool timed = true;
   if (B < 1 || B > HF_MAX_BATCH) return fail(HF_ERR_SHAPE, "B=%d outside [1, %d]", B, HF_MAX_BATCH);
   if (!s_len || !r_len) return fail(HF_ERR_NULL, "s_len / r_len is NULL");
   if (ls.concat) {
@@ -424,6 +440,14 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
   if (bias && (reinterpret_cast<uintptr_t>(bias) & 15u)) return fail(HF_ERR_SHAPE, "bias not 16-byte aligned");
   const int d_in = sender->H * d_h;   // one tap
   const int d_all = ls.n_taps * d_in;  // the map's input size
+  {
+    const size_t want = hf_packed_maps_bytes(L_r, receiver->H * d_h, d_all, dtype);
+    if (A_packed_bytes != want)
+      return fail(HF_ERR_SHAPE,
+                  "A_packed holds %zu bytes, but maps packed by hf_pack_maps for L_r=%d, d_r=%d, "
+                  "d_in=%d, dtype %d hold %zu (with their %d-byte header)", A_packed_bytes, L_r,
+                  receiver->H * d_h, d_all, dtype, want, HF_PACKED_HEADER_BYTES);
+  }
   if (dtype == HF_BF16) {
     if (d_h != 128) return fail(HF_ERR_UNSUPPORTED, "bf16 path needs d_h == 128 (got %d)", d_h);
     const int H = receiver->H;
@@ -486,7 +510,7 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
   std::memset(&a, 0, sizeof a);
   a.S = sender->ptr;
   a.R = receiver->ptr;
-  a.Wp = A_packed;
+  a.Wp = static_cast<const char*>(A_packed) + HF_PACKED_HEADER_BYTES;
   a.bias = bias;
   if (opts) {
     a.inv_r = opts->inv_r;
@@ -568,19 +592,19 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
   }
   hipError_t e = hipSuccess;
   if (a.unrot || a.rot) {
-    TimedLaunch t(HF_KERNEL_ROPE_TABLES, s);
+    TimedLaunch t(HF_KERNEL_ROPE_TABLES, s, timed);
     if (a.unrot) e = hf::launch_rope_table(const_cast<float*>(a.cs_s), rs.P_s, d_h, rope->theta_s, s);
     if (e == hipSuccess && a.rot)
       e = hf::launch_rope_table(const_cast<float*>(a.cs_r), rs.P_r, d_h, rope->theta_r, s);
   }
   if (e != hipSuccess) return hip_fail(e, "RoPE table launch");
   if (a.tile_rec) {
-    TimedLaunch t(HF_KERNEL_TRANSFER_STAGE, s);
+    TimedLaunch t(HF_KERNEL_TRANSFER_STAGE, s, timed);
     e = hf::launch_transfer_stage(dtype, a, s);
   }
   if (e != hipSuccess) return hip_fail(e, "tile staging launch");
   {
-    TimedLaunch t(HF_KERNEL_TRANSFER, s);
+    TimedLaunch t(HF_KERNEL_TRANSFER, s, timed);
     e = hf::launch_transfer(dtype, a, s);
   }
   if (e != hipSuccess) return hip_fail(e, "transfer launch");
@@ -593,31 +617,31 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
                        const int32_t* row_ptr, const int32_t* col, const int32_t* num,
                        const int32_t* den, const int32_t* lo, const int32_t* hi,
                        const int32_t* rem, const int32_t* den_l, const hf_kv_desc* sender,
-                       const hf_kv_desc* receiver, const void* A_packed, const float* bias,
-                       const hf_rope* rope, const hf_transfer_opts* opts, void* workspace,
-                       size_t workspace_bytes, void* stream) {
+                       const hf_kv_desc* receiver, const void* A_packed, size_t A_packed_bytes,
+                       const float* bias, const hf_rope* rope, const hf_transfer_opts* opts,
+                       void* workspace, size_t workspace_bytes, void* stream) {
   LayerSpec ls;
   ls.lo = lo;
   ls.hi = hi;
   ls.rem = rem;
   ls.den_l = den_l;
   return transfer_impl(B, s_len, r_len, row_ptr, col, num, den, ls, sender, receiver, A_packed,
-                       bias, rope, opts, workspace, workspace_bytes, stream);
+                       A_packed_bytes, bias, rope, opts, workspace, workspace_bytes, stream);
 }
 
 int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_len,
                             const int32_t* row_ptr, const int32_t* col, const int32_t* num,
                             const int32_t* den, int32_t n_taps, const int32_t* taps,
                             const hf_kv_desc* sender, const hf_kv_desc* receiver,
-                            const void* A_packed, const float* bias, const hf_rope* rope,
-                            const hf_transfer_opts* opts, void* workspace,
+                            const void* A_packed, size_t A_packed_bytes, const float* bias,
+                            const hf_rope* rope, const hf_transfer_opts* opts, void* workspace,
                             size_t workspace_bytes, void* stream) {
   LayerSpec ls;
   ls.concat = true;
   ls.n_taps = n_taps;
   ls.taps = taps;
   return transfer_impl(B, s_len, r_len, row_ptr, col, num, den, ls, sender, receiver, A_packed,
-                       bias, rope, opts, workspace, workspace_bytes, stream);
+                       A_packed_bytes, bias, rope, opts, workspace, workspace_bytes, stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -12,6 +12,7 @@ namespace hf {
 
 constexpr int kAlignBlock = 256;  // receiver rows per alignment workgroup
 constexpr int kRopeDeltaRows = 16;  // sender RoPE table rows the bf16 kernels always read
+constexpr uint32_t kPackedMagic = 0x4B504648u;  // "HFPK": first word of a packed map buffer
 
 struct AlignArgs {
   const int32_t* s_beg;
@@ -44,7 +45,7 @@ size_t align_workspace_bytes(int nblk);
 struct TransferArgs {
   const void* S;        // sender cache
   void* R;              // receiver cache
-  const void* Wp;       // packed maps
+  const void* Wp;       // packed maps (past the header)
   const float* bias;    // [L_r][2][d_r] or nullptr
   const int32_t* row_ptr;
   const int32_t* col;
@@ -94,7 +95,8 @@ hipError_t launch_transfer_stage(int dtype, const TransferArgs& a, hipStream_t s
 
 hipError_t launch_alignment(const AlignArgs& a, hipStream_t s);
 hipError_t launch_rope_table(float* tab, int P, int d_h, double theta, hipStream_t s);
-hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* A, void* Wp,
+// Writes the header and the packed maps (A_packed: hf_packed_maps_bytes bytes).
+hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* A, void* A_packed,
                             hipStream_t s);
 hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s);
 

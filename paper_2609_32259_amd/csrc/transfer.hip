@@ -85,6 +85,20 @@ __global__ __launch_bounds__(256) void pack_bf16_kernel(const uint16_t* A, uint4
   Wp[idx] = *reinterpret_cast<const uint4*>(A + ((lc * d_r + n) * (long long)d_in + k));
 }
 
+// Header of a packed map buffer: what hf_pack_maps packed, ahead of the data.
+__global__ __launch_bounds__(64) void pack_header_kernel(uint32_t* hdr, int dtype, int L_r,
+                                                         int d_r, int d_in) {
+  const int i = threadIdx.x;
+  uint32_t v = 0;
+  if (i == 0) v = kPackedMagic;
+  if (i == 1) v = 1;  // layout version
+  if (i == 2) v = (uint32_t)dtype;
+  if (i == 3) v = (uint32_t)L_r;
+  if (i == 4) v = (uint32_t)d_r;
+  if (i == 5) v = (uint32_t)d_in;
+  hdr[i] = v;  // 64 words = HF_PACKED_HEADER_BYTES
+}
+
 __global__ __launch_bounds__(256) void copy_f32_kernel(const float4* A, float4* Wp, long long n4) {
   const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
   if (idx < n4) Wp[idx] = A[idx];
@@ -1162,8 +1176,12 @@ hipError_t launch_rope_table(float* tab, int P, int d_h, double theta, hipStream
   return hipGetLastError();
 }
 
-hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* A, void* Wp,
+hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* A, void* A_packed,
                             hipStream_t s) {
+  static_assert(HF_PACKED_HEADER_BYTES == 64 * 4, "header kernel writes 64 words");
+  hipLaunchKernelGGL(pack_header_kernel, dim3(1), dim3(64), 0, s, static_cast<uint32_t*>(A_packed),
+                     dtype, n_lc / 2, d_r, d_in);
+  void* Wp = static_cast<char*>(A_packed) + HF_PACKED_HEADER_BYTES;
   if (dtype == HF_BF16) {
     const long long n = (long long)n_lc * (d_r / 32) * (d_in / 16) * 64;
     if (n > 0)

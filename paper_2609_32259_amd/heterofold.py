@@ -23,6 +23,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libheterofold.so")
 
 HF_OK = 0
+HF_ERR_SHAPE, HF_ERR_MODE = -2, -4
 STATUS = {0: "HF_OK", -1: "HF_ERR_NULL", -2: "HF_ERR_SHAPE", -3: "HF_ERR_OFFSETS",
           -4: "HF_ERR_MODE", -5: "HF_ERR_DTYPE", -6: "HF_ERR_CAPACITY", -7: "HF_ERR_HIP",
           -8: "HF_ERR_UNSUPPORTED"}
@@ -68,7 +69,7 @@ _I32P = C.POINTER(C.c_int32)
 _SIGNATURES = {
     "hf_last_error": (C.c_char_p, []),
     "hf_version": (C.c_int32, []),
-    "hf_alignment_nnz_capacity": (C.c_int64, [C.c_int32, _I32P, _I32P]),
+    "hf_alignment_nnz_capacity": (C.c_int64, [C.c_int32, _I32P, _I32P, C.c_int32]),
     "hf_alignment_workspace_bytes": (C.c_size_t, [C.c_int32, _I32P]),
     "hf_build_alignment": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p,
                                        C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p,
@@ -86,12 +87,13 @@ _SIGNATURES = {
     "hf_transfer_kv": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p, C.c_void_p,
                                    C.c_void_p, _I32P, _I32P, _I32P, _I32P,
                                    C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc), C.c_void_p,
-                                   C.c_void_p, C.POINTER(hf_rope), C.POINTER(hf_transfer_opts),
-                                   C.c_void_p, C.c_size_t, C.c_void_p]),
+                                   C.c_size_t, C.c_void_p, C.POINTER(hf_rope),
+                                   C.POINTER(hf_transfer_opts), C.c_void_p, C.c_size_t,
+                                   C.c_void_p]),
     "hf_transfer_kv_taps": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p,
                                         C.c_void_p, C.c_void_p, C.c_int32, _I32P,
                                         C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc), C.c_void_p,
-                                        C.c_void_p, C.POINTER(hf_rope),
+                                        C.c_size_t, C.c_void_p, C.POINTER(hf_rope),
                                         C.POINTER(hf_transfer_opts), C.c_void_p, C.c_size_t,
                                         C.c_void_p]),
     "hf_recolor_moments_workspace_bytes": (C.c_size_t, [C.c_int64, C.c_int32, C.c_int32]),
@@ -169,6 +171,10 @@ def _stream(stream):
     return C.c_void_p(stream.cuda_stream)
 
 
+def _nbytes(t) -> int:
+    return int(t.numel() * t.element_size())
+
+
 def _dev_i32(t, name):
     torch = _torch()
     if not isinstance(t, torch.Tensor) or t.dtype != torch.int32 or not t.is_cuda \
@@ -185,11 +191,21 @@ def hf_version() -> int:
 # Alignment
 # ---------------------------------------------------------------------------
 
-def hf_alignment_nnz_capacity(s_cu, r_cu) -> int:
-    s_cu, r_cu = _i32(s_cu), _i32(r_cu)
-    n = lib().hf_alignment_nnz_capacity(s_cu.size - 1, _p32(s_cu), _p32(r_cu))
+def _mode_code(mode) -> int:
+    return ALIGN_MODES[mode] if isinstance(mode, str) else int(mode)
+
+
+def hf_alignment_nnz_capacity(s_len, r_len, mode="overlap") -> int:
+    """s_len, r_len: per-sequence token counts [B]."""
+    s_len, r_len = _i32(s_len), _i32(r_len)
+    if s_len.size != r_len.size:
+        raise ValueError("s_len and r_len differ in length")
+    code = _mode_code(mode)
+    n = lib().hf_alignment_nnz_capacity(s_len.size, _p32(s_len), _p32(r_len), code)
     if n < 0:
-        _check(-2, "hf_alignment_nnz_capacity")
+        msg = lib().hf_last_error().decode(errors="replace")
+        st = HF_ERR_MODE if code not in ALIGN_MODES.values() else HF_ERR_SHAPE
+        raise HeteroFoldError(st, "hf_alignment_nnz_capacity", msg)
     return int(n)
 
 
@@ -219,7 +235,7 @@ def hf_build_alignment(s_cu, r_cu, s_beg, s_end, r_beg, r_end, mode="overlap",
     s_cu, r_cu = _i32(s_cu), _i32(r_cu)
     B = s_cu.size - 1
     dev = s_beg.device
-    cap = hf_alignment_nnz_capacity(s_cu, r_cu)
+    cap = hf_alignment_nnz_capacity(np.diff(s_cu), np.diff(r_cu), mode)
     nR = int(r_cu[-1])
     if out is None:
         out = Alignment(torch.empty(nR + 1, dtype=torch.int32, device=dev),
@@ -231,7 +247,7 @@ def hf_build_alignment(s_cu, r_cu, s_beg, s_end, r_beg, r_end, mode="overlap",
         workspace = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
     st = lib().hf_build_alignment(
         B, _p32(s_cu), _p32(r_cu), _dev_i32(s_beg, "s_beg"), _dev_i32(s_end, "s_end"),
-        _dev_i32(r_beg, "r_beg"), _dev_i32(r_end, "r_end"), ALIGN_MODES[mode] if isinstance(mode, str) else int(mode),
+        _dev_i32(r_beg, "r_beg"), _dev_i32(r_end, "r_end"), _mode_code(mode),
         _dev_i32(out.row_ptr, "row_ptr"), _dev_i32(out.col, "col"), _dev_i32(out.num, "num"),
         _dev_i32(out.den, "den"), int(out.col.numel()), C.c_void_p(workspace.data_ptr()),
         int(workspace.numel() * workspace.element_size()), _stream(stream))
@@ -284,14 +300,16 @@ def hf_packed_maps_bytes(L_r, d_r, d_in, dtype) -> int:
 
 def hf_pack_maps(A, out=None, stream=None):
     """A: contiguous CUDA tensor [L_r, 2, d_r, d_in] (bf16 or fp32).  Returns
-    the packed maps as a flat tensor of the same dtype."""
+    the packed buffer (header + maps) as a flat uint8 tensor of
+    hf_packed_maps_bytes bytes."""
     torch = _torch()
     if A.dim() != 4 or A.shape[1] != 2 or not A.is_contiguous() or not A.is_cuda:
         raise TypeError("A must be a contiguous CUDA tensor [L_r, 2, d_r, d_in]")
     L_r, _, d_r, d_in = A.shape
     code = _dtype_code(A)
     if out is None:
-        out = torch.empty(A.numel(), dtype=A.dtype, device=A.device)
+        out = torch.empty(hf_packed_maps_bytes(L_r, d_r, d_in, code), dtype=torch.uint8,
+                          device=A.device)
     st = lib().hf_pack_maps(L_r, d_r, d_in, code, C.c_void_p(A.data_ptr()),
                             C.c_void_p(out.data_ptr()), _stream(stream))
     _check(st, "hf_pack_maps")
@@ -374,7 +392,7 @@ def hf_transfer_kv(s_len, r_len, alignment: Alignment, layer_map, S, R, A_packed
         s_len.size, _p32(s_len), _p32(r_len), _dev_i32(alignment.row_ptr, "row_ptr"),
         _dev_i32(alignment.col, "col"), _dev_i32(alignment.num, "num"),
         _dev_i32(alignment.den, "den"), _p32(lo), _p32(hi), _p32(rem), _p32(den_l),
-        C.byref(sd), C.byref(rd), C.c_void_p(A_packed.data_ptr()),
+        C.byref(sd), C.byref(rd), C.c_void_p(A_packed.data_ptr()), _nbytes(A_packed),
         C.c_void_p(bias.data_ptr()) if bias is not None else None,
         C.byref(rs) if rs is not None else None,
         C.byref(os_) if os_ is not None else None,
@@ -407,7 +425,7 @@ def hf_transfer_kv_taps(s_len, r_len, alignment: Alignment, taps, S, R, A_packed
         s_len.size, _p32(s_len), _p32(r_len), _dev_i32(alignment.row_ptr, "row_ptr"),
         _dev_i32(alignment.col, "col"), _dev_i32(alignment.num, "num"),
         _dev_i32(alignment.den, "den"), int(taps.shape[1]), _p32(taps),
-        C.byref(sd), C.byref(rd), C.c_void_p(A_packed.data_ptr()),
+        C.byref(sd), C.byref(rd), C.c_void_p(A_packed.data_ptr()), _nbytes(A_packed),
         C.c_void_p(bias.data_ptr()) if bias is not None else None,
         C.byref(rs) if rs is not None else None,
         C.byref(os_) if os_ is not None else None,

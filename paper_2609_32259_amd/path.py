@@ -48,7 +48,7 @@ class TransferPath:
         self.s_beg, self.s_end = as_dev(seg.s_beg), as_dev(seg.s_end)
         self.r_beg, self.r_end = as_dev(seg.r_beg), as_dev(seg.r_end)
         self.s_len, self.r_len = seg.s_len, seg.r_len
-        cap = hf.hf_alignment_nnz_capacity(seg.s_cu, seg.r_cu)
+        cap = hf.hf_alignment_nnz_capacity(seg.s_len, seg.r_len, mode)
         nR = int(seg.r_cu[-1])
         self.alignment = hf.Alignment(
             torch.zeros(nR + 1, dtype=torch.int32, device=dev),

@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(L):
 
 
 def test_version(L):
-    assert hf.hf_version() == 1
+    assert hf.hf_version() == 2
 
 
 @pytest.mark.parametrize("L_s,L_r", [(4, 6), (32, 40), (32, 28), (28, 32), (1, 3), (5, 1), (7, 7)])
@@ -68,9 +68,18 @@ def test_validate_offsets_host(L):
 
 
 def test_nnz_capacity(L):
-    assert hf.hf_alignment_nnz_capacity([0, 10, 25], [0, 8, 20]) == 25 + 40
-    with pytest.raises(hf.HeteroFoldError):
-        hf.hf_alignment_nnz_capacity([1, 10], [0, 8])
+    assert hf.hf_alignment_nnz_capacity([10, 15], [8, 12]) == 25 + 40
+    assert hf.hf_alignment_nnz_capacity([10, 15], [8, 12], "ta") == 20
+    assert hf.hf_alignment_nnz_capacity([0], [0]) == 0
+    with pytest.raises(hf.HeteroFoldError) as ei:
+        hf.hf_alignment_nnz_capacity([-1, 10], [0, 8])
+    assert ei.value.status == -2
+    with pytest.raises(hf.HeteroFoldError) as ei:
+        hf.hf_alignment_nnz_capacity([1], [1], 7)
+    assert ei.value.status == -4
+    s, r = np.array([3], np.int32), np.array([2], np.int32)
+    assert L.hf_alignment_nnz_capacity(0, _p(s), _p(r), 0) == -1
+    assert L.hf_alignment_nnz_capacity(1, None, _p(r), 0) == -1
 
 
 def _p(a):
@@ -94,7 +103,8 @@ def test_alignment_host_validation(L):
     assert call(args(mode=5)) == -4
     assert call(args(rp=None)) == -1
     assert call(args(col=None)) == -1
-    assert call(args(cap=27)) == -6
+    assert call(args(cap=27)) == -6           # overlap needs T_s + 2 T_r = 28
+    assert call(args(cap=8, mode=1)) == -6    # TA needs T_r = 9
     assert call(args(ws=None)) == -1
     assert call(args(wsb=1)) == -6
     bad = np.array([0, 0], np.int32)
@@ -117,18 +127,24 @@ def test_transfer_host_validation(L):
     lt = [np.ascontiguousarray(x, dtype=np.int32) for x in lm.interp2(4, 6)]
     fake = C.c_void_p(0x1000)
 
-    def call(sd=None, rd=None, B=1, sl=s_len, rl=r_len, table=lt, A=fake, rope=None, ws=None, wsb=0,
-             rp=fake, opts=None):
+    def call(sd=None, rd=None, B=1, sl=s_len, rl=r_len, table=lt, A=fake, Ab=None, rope=None,
+             ws=None, wsb=0, rp=fake, opts=None):
         sd = sd or _desc()
         rd = rd or _desc(L_=6)
+        if Ab is None:
+            Ab = L.hf_packed_maps_bytes(rd.L, rd.H * rd.d_h, sd.H * sd.d_h, sd.dtype)
         return L.hf_transfer_kv(B, _p(sl), _p(rl), rp, fake, fake, fake, *[_p(t) for t in table],
-                                C.byref(sd), C.byref(rd), A, None,
+                                C.byref(sd), C.byref(rd), A, Ab, None,
                                 C.byref(rope) if rope is not None else None,
                                 C.byref(opts) if opts is not None else None, ws, wsb, None)
 
     assert call(B=0) == -2
     assert call(rp=None) == -1
     assert call(A=None) == -1
+    unpacked = 6 * 2 * 1024 * 1024 * 2                         # A [L_r][2][d_r][d_in], bf16
+    assert call(Ab=unpacked) == -2                             # an unpacked map is refused
+    assert "hf_pack_maps" in L.hf_last_error().decode()
+    assert call(Ab=unpacked + 256 + 2) == -2
     assert call(sd=_desc(ptr=0)) == -1
     assert call(sd=_desc(dtype=0)) == -5                       # dtypes differ
     assert call(sd=_desc(dtype=9)) == -5
@@ -181,8 +197,9 @@ def test_transfer_workspace_records(L):
 
     def call(ws, n):
         sd, rd = _desc(), _desc(L_=6)
+        Ab = L.hf_packed_maps_bytes(6, 1024, 1024, 1)
         return L.hf_transfer_kv(3, _p(s_len), _p(r_len), fake, fake, fake, fake,
-                                *[_p(t) for t in lt], C.byref(sd), C.byref(rd), fake, None,
+                                *[_p(t) for t in lt], C.byref(sd), C.byref(rd), fake, Ab, None,
                                 None, None, ws, n, None)
 
     assert call(None, 0) == -1                       # records need a workspace
@@ -196,7 +213,9 @@ def test_pack_host_validation(L):
     assert L.hf_pack_maps(2, 128, 1024, 3, fake, C.c_void_p(0x100000), None) == -5
     assert L.hf_pack_maps(2, 128, 1024, 1, None, C.c_void_p(0x100000), None) == -1
     assert L.hf_pack_maps(2, 128, 128, 1, fake, C.c_void_p(0x1000 + 64), None) == -2  # overlap
-    assert hf.hf_packed_maps_bytes(40, 1024, 1024, 1) == 40 * 2 * 1024 * 1024 * 2
+    assert hf.hf_packed_maps_bytes(40, 1024, 1024, 1) == 256 + 40 * 2 * 1024 * 1024 * 2
+    assert hf.hf_packed_maps_bytes(40, 1024, 1024, 0) == 256 + 40 * 2 * 1024 * 1024 * 4
+    assert hf.hf_packed_maps_bytes(40, 1024, 1024, 5) == 0
 
 
 def test_profiler_host_calls(L):
@@ -234,9 +253,10 @@ def test_transfer_taps_host_validation(L):
     def call(n=3, tp=taps, sd=None, rd=None):
         sd = sd or _desc()
         rd = rd or _desc(L_=6)
+        Ab = L.hf_packed_maps_bytes(rd.L, rd.H * rd.d_h, max(n, 1) * sd.H * sd.d_h, sd.dtype)
         return L.hf_transfer_kv_taps(1, _p(s_len), _p(r_len), fake, fake, fake, fake, n,
                                      _p(tp) if tp is not None else None, C.byref(sd),
-                                     C.byref(rd), fake, None, None, None, None, 0, None)
+                                     C.byref(rd), fake, Ab, None, None, None, None, 0, None)
 
     assert call(tp=None) == -1
     assert call(n=0) == -2
@@ -313,3 +333,4 @@ def test_recolor_host_validation(L):
     assert gemm(ak=1, lda=3) == -2
     assert gemm(ldd=3) == -2
     assert gemm(beta=1.0, Cp=fake, ldc=3) == -2
+
