@@ -300,6 +300,33 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
                        void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * hf_transfer_kv for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Arguments, results and errors as hf_transfer_kv, without the workspace: the
+ * scratch it needs (the RoPE tables, one 8 KB staging record per 64-row
+ * receiver tile, a work counter; hf_transfer_workspace_bytes gives the amount)
+ * lives in a device array of HF_NOALLOC_SCRATCH_BYTES inside the library,
+ * which each GPU the library runs on holds from load until the process ends.
+ * A transfer that needs more returns HF_ERR_CAPACITY before anything is
+ * launched (at 64 MiB: a 32K-token sequence needs about 34 MB, four of them
+ * about 47 MB).  The call allocates nothing (no hipMalloc / hipFree, no
+ * profiler events: its launches are not timed by hf_profiler_*); its first
+ * call on a device resolves the array's device address.  Every call on one
+ * GPU shares that GPU's array: calls that overlap on one GPU (different
+ * streams, different host threads) race and must be serialized by the
+ * caller.  Nothing in the array has to start at zero: each call writes what
+ * it reads before reading it.
+ */
+#define HF_NOALLOC_SCRATCH_BYTES (64 << 20)
+int32_t hf_transfer_kv_noalloc(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                               const int32_t* row_ptr, const int32_t* col, const int32_t* num,
+                               const int32_t* den, const int32_t* lo, const int32_t* hi,
+                               const int32_t* rem, const int32_t* den_l,
+                               const hf_kv_desc* sender, const hf_kv_desc* receiver,
+                               const void* A_packed, size_t A_packed_bytes, const float* bias,
+                               const hf_rope* rope, const hf_transfer_opts* opts, void* stream);
+
+/*
  * hf_transfer_kv for maps over concatenated sender layers (Sec. 3.1 Eq. 2,
  * with the folded map of Eq. 9): receiver layer l reads the n_taps sender
  * layers taps[l][0..n_taps) without interpolation, and its map sees their

@@ -411,13 +411,16 @@ struct LayerSpec {
   const int32_t* taps = nullptr;  // [L_r][n_taps]
 };
 
+// timed: bracket the launches with profiler events (which create HIP events);
+// the no-allocation entry point passes false.
 int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
                       const int32_t* row_ptr, const int32_t* col, const int32_t* num,
                       const int32_t* den, const LayerSpec& ls, const hf_kv_desc* sender,
                       const hf_kv_desc* receiver, const void* A_packed, size_t A_packed_bytes,
                       const float* bias, const hf_rope* rope, const hf_transfer_opts* opts,
-                      void* workspace, size_t workspace_bytes, void* stream) {
-  const bool timed = true;
+                      void* workspace, size_t workspace_bytes, void* stream,
+                      bool noalloc = false) {
+  const bool timed = !noalloc;
   if (B < 1 || B > HF_MAX_BATCH) return fail(HF_ERR_SHAPE, "B=%d outside [1, %d]", B, HF_MAX_BATCH);
   if (!s_len || !r_len) return fail(HF_ERR_NULL, "s_len / r_len is NULL");
   if (ls.concat) {
@@ -498,7 +501,12 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
   if ((st = rope_sizes(B, s_len, r_len, rope, rs))) return st;
   const size_t rec_off = rope_bytes(rs.P_s, d_h) + rope_bytes(rs.P_r, d_h);
   const size_t ws_need = rec_off + record_bytes(B, r_len, sender, receiver);
-  if (ws_need > 0) {
+  if (noalloc && ws_need > HF_NOALLOC_SCRATCH_BYTES)
+    return fail(HF_ERR_CAPACITY,
+                "this transfer needs %zu bytes of scratch, more than the %d bytes "
+                "hf_transfer_kv_noalloc holds; use hf_transfer_kv with a workspace",
+                ws_need, HF_NOALLOC_SCRATCH_BYTES);
+  if (ws_need > 0 && !noalloc) {
     if (!workspace) return fail(HF_ERR_NULL, "workspace is NULL");
     if (workspace_bytes < ws_need)
       return fail(HF_ERR_CAPACITY, "workspace %zu bytes < required %zu", workspace_bytes, ws_need);
@@ -568,6 +576,11 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
     a.wlo[j] = (float)((double)(ls.den_l[j] - ls.rem[j]) / (double)ls.den_l[j]);
     a.whi[j] = (float)((double)ls.rem[j] / (double)ls.den_l[j]);
   }
+  if (noalloc && ws_need > 0) {  // every host check has passed: the library's scratch array
+    workspace = nullptr;
+    const hipError_t se = hf::noalloc_scratch(&workspace);
+    if (se != hipSuccess) return hip_fail(se, "scratch symbol address");
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* w = static_cast<char*>(workspace);
   if (rope && rope->unrotate_sender_k && rs.P_s > 0) {
@@ -627,6 +640,22 @@ int32_t hf_transfer_kv(int32_t B, const int32_t* s_len, const int32_t* r_len,
   ls.den_l = den_l;
   return transfer_impl(B, s_len, r_len, row_ptr, col, num, den, ls, sender, receiver, A_packed,
                        A_packed_bytes, bias, rope, opts, workspace, workspace_bytes, stream);
+}
+
+int32_t hf_transfer_kv_noalloc(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                               const int32_t* row_ptr, const int32_t* col, const int32_t* num,
+                               const int32_t* den, const int32_t* lo, const int32_t* hi,
+                               const int32_t* rem, const int32_t* den_l,
+                               const hf_kv_desc* sender, const hf_kv_desc* receiver,
+                               const void* A_packed, size_t A_packed_bytes, const float* bias,
+                               const hf_rope* rope, const hf_transfer_opts* opts, void* stream) {
+  LayerSpec ls;
+  ls.lo = lo;
+  ls.hi = hi;
+  ls.rem = rem;
+  ls.den_l = den_l;
+  return transfer_impl(B, s_len, r_len, row_ptr, col, num, den, ls, sender, receiver, A_packed,
+                       A_packed_bytes, bias, rope, opts, nullptr, 0, stream, /*noalloc=*/true);
 }
 
 int32_t hf_transfer_kv_taps(int32_t B, const int32_t* s_len, const int32_t* r_len,

@@ -99,6 +99,9 @@ hipError_t launch_rope_table(float* tab, int P, int d_h, double theta, hipStream
 hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* A, void* A_packed,
                             hipStream_t s);
 hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s);
+// Device address of the no-allocation scratch (HF_NOALLOC_SCRATCH_BYTES) on the
+// current device; resolved once per device.
+hipError_t noalloc_scratch(void** ptr);
 
 // Offline map construction (fp64).  Workspace layouts are private to recolor.hip.
 int moments_chunks(long long n);

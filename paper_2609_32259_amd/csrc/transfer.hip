@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <limits.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "hf_internal.h"
@@ -1194,6 +1195,35 @@ hipError_t launch_pack_maps(int dtype, int n_lc, int d_r, int d_in, const void* 
                          static_cast<const float4*>(A), static_cast<float4*>(Wp), n4);
   }
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Scratch of hf_transfer_kv_noalloc: the workspace of a transfer (RoPE
+// tables, staged tile records, work counter) in a file-scope device array, so
+// that the call allocates nothing.  Each device holds its own copy from module
+// load until the process ends.  Host code never passes the array's name to a
+// kernel: it resolves the device address once per device and uses that.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[HF_NOALLOC_SCRATCH_BYTES];
+
+hipError_t noalloc_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* per_device[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(mu);
+  if (!per_device[dev]) {  // first call on this device, with it current
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    per_device[dev] = p;
+  }
+  *ptr = per_device[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s) {

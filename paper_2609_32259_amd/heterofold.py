@@ -90,6 +90,12 @@ _SIGNATURES = {
                                    C.c_size_t, C.c_void_p, C.POINTER(hf_rope),
                                    C.POINTER(hf_transfer_opts), C.c_void_p, C.c_size_t,
                                    C.c_void_p]),
+    "hf_transfer_kv_noalloc": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, _I32P, _I32P, _I32P, _I32P,
+                                           C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc),
+                                           C.c_void_p, C.c_size_t, C.c_void_p,
+                                           C.POINTER(hf_rope), C.POINTER(hf_transfer_opts),
+                                           C.c_void_p]),
     "hf_transfer_kv_taps": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p,
                                         C.c_void_p, C.c_void_p, C.c_int32, _I32P,
                                         C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc), C.c_void_p,
@@ -400,6 +406,31 @@ def hf_transfer_kv(s_len, r_len, alignment: Alignment, layer_map, S, R, A_packed
         int(workspace.numel() * workspace.element_size()) if workspace is not None else 0,
         _stream(stream))
     _check(st, "hf_transfer_kv")
+    return R
+
+
+def hf_transfer_kv_noalloc(s_len, r_len, alignment: Alignment, layer_map, S, R, A_packed,
+                           bias=None, rope=None, stream=None, opts=None):
+    """hf_transfer_kv without a workspace: the library's own device scratch
+    array holds it, and the call allocates nothing (arguments as
+    hf_transfer_kv)."""
+    torch = _torch()
+    s_len, r_len = _i32(s_len), _i32(r_len)
+    lo, hi, rem, den_l = (_i32(x) for x in layer_map)
+    sd, rd = kv_desc(S), kv_desc(R)
+    rs, keep = _rope_struct(rope)
+    os_ = _opts_struct(opts)
+    if bias is not None and (bias.dtype != torch.float32 or not bias.is_contiguous()):
+        raise TypeError("bias must be a contiguous fp32 tensor [L_r, 2, d_r]")
+    st = lib().hf_transfer_kv_noalloc(
+        s_len.size, _p32(s_len), _p32(r_len), _dev_i32(alignment.row_ptr, "row_ptr"),
+        _dev_i32(alignment.col, "col"), _dev_i32(alignment.num, "num"),
+        _dev_i32(alignment.den, "den"), _p32(lo), _p32(hi), _p32(rem), _p32(den_l),
+        C.byref(sd), C.byref(rd), C.c_void_p(A_packed.data_ptr()), _nbytes(A_packed),
+        C.c_void_p(bias.data_ptr()) if bias is not None else None,
+        C.byref(rs) if rs is not None else None,
+        C.byref(os_) if os_ is not None else None, _stream(stream))
+    _check(st, "hf_transfer_kv_noalloc")
     return R
 
 

@@ -334,3 +334,30 @@ def test_recolor_host_validation(L):
     assert gemm(ldd=3) == -2
     assert gemm(beta=1.0, Cp=fake, ldc=3) == -2
 
+
+def test_transfer_noalloc_host_validation(L):
+    # Host checks run before any HIP call; a transfer whose scratch exceeds the
+    # library's array is refused with HF_ERR_CAPACITY.
+    s_len = np.array([64], np.int32)
+    r_len = np.array([60], np.int32)
+    lt = [np.ascontiguousarray(x, dtype=np.int32) for x in lm.interp2(4, 6)]
+    fake = C.c_void_p(0x1000)
+    sd, rd = _desc(), _desc(L_=6)
+    Ab = L.hf_packed_maps_bytes(6, 1024, 1024, 1)
+
+    def call(rope=None, Ab=Ab, sd=sd, rp=fake):
+        return L.hf_transfer_kv_noalloc(1, _p(s_len), _p(r_len), rp, fake, fake, fake,
+                                        *[_p(t) for t in lt], C.byref(sd), C.byref(rd), fake, Ab,
+                                        None, C.byref(rope) if rope is not None else None, None,
+                                        None)
+
+    assert call(rp=None) == -1
+    assert call(Ab=Ab - 256) == -2                              # unpacked map
+    assert call(sd=_desc(d=64)) == -2                           # d_h differs
+    far = np.array([100_000_000], np.int32)                     # RoPE tables past 64 MiB
+    r, keep = hf.make_rope(5e5, 1e9, pos0_s=far)
+    assert call(rope=r) == -6
+    assert "hf_transfer_kv_noalloc" in L.hf_last_error().decode()
+    r0, keep0 = hf.make_rope(5e5, 1e9)
+    assert 0 < L.hf_transfer_workspace_bytes(1, _p(s_len), _p(r_len), C.byref(sd), C.byref(rd),
+                                             C.byref(r0)) < 64 << 20
