@@ -93,17 +93,75 @@ def kernel_traffic(cfg):
         return None
 
 
+def cpu_model() -> str:
+    """The host CPU's model name and logical CPU count, from /proc/cpuinfo."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{name}, {os.cpu_count()} logical CPUs"
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def cpu_baseline_full(wl):
+    """The fp64 oracle over the whole step at full length: the alignment of
+    the batch and every receiver layer, K and V, each layer from its own sender
+    taps (as ``cpu_baseline`` does for one layer).  One run, minutes of CPU."""
+    from oracle import alignment as al
+    from oracle import layer_map as lm
+    from oracle import transfer as tr
+    cfg, seg = wl.cfg, wl.seg
+    if cfg.layer_map != "interp2" or wl.opts is not None:
+        raise SystemExit("--cpu-baseline-full covers the interpolating map without options")
+    lt = lm.interp2(cfg.L_s, cfg.L_r)
+    t_total = 0.0
+    for b in range(seg.batch):
+        t0 = time.perf_counter()
+        csr = al.build_alignment(*seg.seq(b), "overlap")
+        t_total += time.perf_counter() - t0
+        T_s = int(seg.s_len[b])
+        rp = None if wl.rope is None else dict(wl.rope, pos0_s=0, pos0_r=0)
+        for layer in range(cfg.L_r):
+            lo, hi = int(lt[0][layer]), int(lt[1][layer])
+            taps = [lo] if lt[2][layer] == 0 else [lo, hi]
+            sub = (np.array([0]), np.array([len(taps) - 1]), lt[2][layer:layer + 1],
+                   lt[3][layer:layer + 1])
+            S = wl.S[b, taps, :, :, :T_s, :].float().cpu().numpy().astype(np.float64)
+            A = wl.A[layer:layer + 1].float().cpu().numpy().astype(np.float64)
+            bias = wl.bias[layer:layer + 1].float().cpu().numpy().astype(np.float64)
+            t0 = time.perf_counter()
+            tr.transfer(S, sub, csr, A, bias, rp, H_r=cfg.H_r)
+            t_total += time.perf_counter() - t0
+            del S
+            log(f"[bench] oracle b={b} layer {layer}: {t_total:.1f} s so far")
+    T_r = int(seg.r_len.sum())
+    return {"value": T_r / t_total, "unit": "tokens/s", "cores": blas_threads(),
+            "kind": "oracle", "cpu": cpu_model(),
+            "sample": (f"fp64 NumPy oracle, the whole step at full length: overlap alignment and "
+                       f"all {cfg.L_r} receiver layers, K and V, of {T_r} receiver tokens: "
+                       f"{t_total:.1f} s of oracle time in one run (host copies of the cache "
+                       f"excluded)")}
+
+
 def cpu_baseline(wl, budget_s=30.0):
     """Time the fp64 oracle on the host: the full alignment of the batch plus
     one receiver layer (K and V) at full length; scale to the whole step."""
     from oracle import alignment as al
     from oracle import layer_map as lm
     from oracle import transfer as tr
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
+    threads = blas_threads()
     cfg, seg = wl.cfg, wl.seg
     t0 = time.perf_counter()
     csr = [al.build_alignment(*seg.seq(b), "overlap") for b in range(seg.batch)]
@@ -140,6 +198,7 @@ def cpu_baseline(wl, budget_s=30.0):
     est = t_align + cfg.L_r * t_layer
     T_r = int(seg.r_len.sum())
     return {"value": T_r / est, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": (f"fp64 NumPy oracle: full overlap alignment of the batch ({t_align:.2f} s) "
                        f"+ receiver layer {layer} K and V at full length ({t_layer:.2f} s), "
                        f"scaled to {cfg.L_r} layers: {est:.1f} s per step of {T_r} receiver tokens")}
@@ -149,11 +208,7 @@ def cpu_baseline_calib(x, y, w, p, rank, budget_rows=16384):
     """The fp64 oracle on the host: weighted moments of the first budget_rows
     samples (scaled to all n) plus the Recolor solve and the fold on them."""
     from oracle import recolor as rc
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
+    threads = blas_threads()
     n = int(x.shape[0])
     k = min(n, budget_rows)
     X = x[:k].double().cpu().numpy()
@@ -171,6 +226,7 @@ def cpu_baseline_calib(x, y, w, p, rank, budget_rows=16384):
     t_solve = time.perf_counter() - t0
     est = t_mom * n / k + t_solve
     return {"value": n / est, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": (f"fp64 NumPy oracle: weighted moments of {k} samples ({t_mom:.2f} s, "
                        f"scaled to {n}) + Recolor solve and rank-{rank} fold ({t_solve:.2f} s): "
                        f"{est:.1f} s per map")}
@@ -293,11 +349,31 @@ def run_gemm_yardstick(args, cfg):
     ms = np.array([a.elapsed_time(b) for a, b in ev])
     flops = 2.0 * L * M * K * N
     tf = flops / (ms.mean() * 1e-3) / 1e12
+    del X, W, Y
+    # The library's best case on this chip: one square 8192^3 product.
+    S = 8192
+    Xs = torch.randn((S, S), generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    Ws = torch.randn((S, S), generator=g, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    Ys = torch.empty((S, S), device="cuda", dtype=torch.bfloat16)
+    for _ in range(args.warmup):
+        torch.matmul(Xs, Ws, out=Ys)
+    torch.cuda.synchronize()
+    ev2 = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in ev2:
+        a.record()
+        torch.matmul(Xs, Ws, out=Ys)
+        b.record()
+    torch.cuda.synchronize()
+    ms2 = np.array([a.elapsed_time(b) for a, b in ev2])
+    tf2 = 2.0 * S ** 3 / (ms2.mean() * 1e-3) / 1e12
     out = {"yardstick": "torch.bmm bf16 (hipBLASLt)", "workload": cfg.name,
            "shape": {"batch": L, "M": M, "K": K, "N": N}, "steps": args.steps,
            "ms_mean": round(float(ms.mean()), 4), "ms_median": round(float(np.median(ms)), 4),
            "ms_min": round(float(ms.min()), 4), "tflops": round(tf, 1),
-           "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+           "frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+           "square_8192": {"ms_mean": round(float(ms2.mean()), 4), "tflops": round(tf2, 1),
+                           "frac_of_peak": round(tf2 / PEAK_BF16_TFLOPS, 4)}}
     print(json.dumps(out), flush=True)
 
 
@@ -309,6 +385,12 @@ def main():
     ap.add_argument("--workload", default="14b-32k")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--T-s", dest="T_s", type=int, default=None,
+                    help="sender tokens per sequence, overriding the workload's (the "
+                         "reverse-b4 context sweep: 1024, 4096, 16384, 32768)")
+    ap.add_argument("--cpu-baseline-full", action="store_true",
+                    help="time the oracle over the whole step at full length instead of "
+                         "one layer scaled (minutes of CPU)")
     ap.add_argument("--gemm-yardstick", action="store_true",
                     help="time a plain hipBLASLt bf16 GEMM of the workload's shape instead")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -339,6 +421,10 @@ def main():
         run_calibration(args, synth.CALIB_CONFIGS[args.workload])
         return
     cfg = synth.CONFIGS[args.workload]
+    if args.T_s is not None:
+        import re
+        name = re.sub(r" T_s=\d+", "", cfg.name)
+        cfg = cfg.with_(T_s=args.T_s, name=f"{name} T_s={args.T_s}")
     if args.gemm_yardstick:
         run_gemm_yardstick(args, cfg)
         return
@@ -376,10 +462,17 @@ def main():
         f"rope tables {r_ms / max(r_n, 1):.3f} ms; tile staging {g_ms / max(g_n, 1):.3f} ms")
 
     flops, bytes_alg = algorithmic_cost(cfg, wl.seg)
-    achieved = flops / (k_avg * 1e-3) / 1e12
     traffic = kernel_traffic(cfg)
-    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+    # The binding roof: matrix-core time against HBM time of the algorithmic work.
+    if bytes_alg / (PEAK_HBM_GBS * 1e9) > flops / (PEAK_BF16_TFLOPS * 1e12):
+        bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
+        achieved = bytes_alg / (k_avg * 1e-3) / 1e9
+    else:
+        bound, unit, peak = "mfma", "TFLOP/s", PEAK_BF16_TFLOPS
+        achieved = flops / (k_avg * 1e-3) / 1e12
+    roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
+            "tflops": round(flops / (k_avg * 1e-3) / 1e12, 2), "algorithmic_flops": flops,
             "kernel": kernel_name(cfg), "kernel_ms": round(k_avg, 4),
             "kernel_ms_median": round(k_med, 4), "kernel_ms_min": round(k_min, 4),
             "kernel_ms_p90": round(k_p90, 4),
@@ -388,7 +481,10 @@ def main():
             "algorithmic_bytes": bytes_alg,
             "hbm_GBps_algorithmic": round(bytes_alg / (k_avg * 1e-3) / 1e9, 1)}
     cpu = None
-    if not args.no_cpu_baseline:
+    if args.cpu_baseline_full:
+        log("[bench] timing the CPU oracle over the whole step at full length")
+        cpu = cpu_baseline_full(wl)
+    elif not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a bounded sample")
         cpu = cpu_baseline(wl)
     out = {
