@@ -40,6 +40,8 @@ CALIB_METRIC = "calibration samples/sec for one map (moments + Recolor + fold, f
 METRIC = "receiver KV tokens/sec (all layers, K+V) at 32K; % of MFMA/HBM roofline"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "transfer_bf16_14b_32k_traffic.json")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_32259_amd", "csrc", "transfer.hip")
+STAGED_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "staged_gemm_14b_32k_traffic.json")
+STAGED_SOURCE = os.path.join(ROOT, "paper_2609_32259_amd", "csrc", "staged.hip")
 
 
 def log(*a):
@@ -78,14 +80,14 @@ def kernel_name(cfg):
     return f"transfer_bf16_direct_kernel<{cfg.H_r}>"
 
 
-def kernel_traffic(cfg):
-    """HBM bytes per transfer launch from the committed rocprofv3 counter
-    summary, or None if there is none for this workload or the kernel source
-    changed since."""
+def kernel_traffic(cfg, staged=False):
+    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
+    counter summary, or None if there is none for this workload or the kernel
+    source changed since."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(STAGED_TRAFFIC_FILE if staged else TRAFFIC_FILE) as f:
             rec = json.load(f)
-        src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+        src = hashlib.sha256(open(STAGED_SOURCE if staged else KERNEL_SOURCE, "rb").read()).hexdigest()
         if rec.get("kernel_source_sha256") != src or rec.get("workload_name") != cfg.name:
             return None
         return rec.get("bytes_per_launch")
@@ -385,6 +387,10 @@ def main():
     ap.add_argument("--workload", default="14b-32k")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--path", choices=("auto", "fused", "staged"), default="auto",
+                    help="transfer path: the library's staged path (build the aligned features "
+                         "into the workspace, then a separate multiply) where the shape allows "
+                         "it (auto), or force one")
     ap.add_argument("--T-s", dest="T_s", type=int, default=None,
                     help="sender tokens per sequence, overriding the workload's (the "
                          "reverse-b4 context sweep: 1024, 4096, 16384, 32768)")
@@ -430,8 +436,9 @@ def main():
         return
     log(f"[bench] workload {cfg.name}: generating inputs on the GPU")
     wl = synth.make_workload(cfg, seed=args.seed, device="cuda")
+    staged = {"auto": None, "fused": False, "staged": True}[args.path]
     path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r,
-                        layer_map=cfg.layer_map, opts=wl.opts)
+                        layer_map=cfg.layer_map, opts=wl.opts, staged=staged)
     torch.cuda.synchronize()
     T_r = int(wl.seg.r_len.sum())
     T_s = int(wl.seg.s_len.sum())
@@ -450,19 +457,28 @@ def main():
     t1 = time.perf_counter()
     hf.hf_profiler_enable(False)
     ms_step = (t1 - t0) * 1e3 / args.steps
-    k_ms, k_n = hf.hf_profiler_query(hf.HF_KERNEL_TRANSFER)
+    sg_ms, sg_n = hf.hf_profiler_query(hf.HF_KERNEL_STAGED_GEMM)
+    sb_ms, sb_n = hf.hf_profiler_query(hf.HF_KERNEL_STAGED_BUILD)
+    ran_staged = sg_n > 0
+    # The dominant kernel: the fused transfer kernel, or on the staged path its multiply.
+    dom = hf.HF_KERNEL_STAGED_GEMM if ran_staged else hf.HF_KERNEL_TRANSFER
+    k_ms, k_n = hf.hf_profiler_query(dom)
     a_ms, a_n = hf.hf_profiler_query(hf.HF_KERNEL_ALIGNMENT)
     r_ms, r_n = hf.hf_profiler_query(hf.HF_KERNEL_ROPE_TABLES)
     g_ms, g_n = hf.hf_profiler_query(hf.HF_KERNEL_TRANSFER_STAGE)
     k_avg = k_ms / max(k_n, 1)
-    ks = hf.hf_profiler_samples(hf.HF_KERNEL_TRANSFER).astype(np.float64)
+    b_avg = sb_ms / max(sb_n, 1)
+    ks = hf.hf_profiler_samples(dom).astype(np.float64)
     k_med, k_min, k_p90 = (float(np.median(ks)), float(ks.min()), float(np.percentile(ks, 90)))
-    log(f"[bench] step {ms_step:.3f} ms; transfer kernel mean {k_avg:.3f} ms, median {k_med:.3f}, "
-        f"min {k_min:.3f}, p90 {k_p90:.3f} (x{k_n}); alignment {a_ms / max(a_n, 1):.3f} ms; "
-        f"rope tables {r_ms / max(r_n, 1):.3f} ms; tile staging {g_ms / max(g_n, 1):.3f} ms")
+    log(f"[bench] path {'staged' if ran_staged else 'fused'}; step {ms_step:.3f} ms; "
+        f"{'multiply' if ran_staged else 'transfer'} kernel mean {k_avg:.3f} ms, median {k_med:.3f}, "
+        f"min {k_min:.3f}, p90 {k_p90:.3f} (x{k_n}); "
+        + (f"staged build {b_avg:.3f} ms; " if ran_staged else "")
+        + f"alignment {a_ms / max(a_n, 1):.3f} ms; rope tables {r_ms / max(r_n, 1):.3f} ms; "
+        f"tile staging {g_ms / max(g_n, 1):.3f} ms")
 
     flops, bytes_alg = algorithmic_cost(cfg, wl.seg)
-    traffic = kernel_traffic(cfg)
+    traffic = kernel_traffic(cfg, staged=ran_staged)
     # The binding roof: matrix-core time against HBM time of the algorithmic work.
     if bytes_alg / (PEAK_HBM_GBS * 1e9) > flops / (PEAK_BF16_TFLOPS * 1e12):
         bound, unit, peak = "hbm", "GB/s", PEAK_HBM_GBS
@@ -473,13 +489,20 @@ def main():
     roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak,
             "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
             "tflops": round(flops / (k_avg * 1e-3) / 1e12, 2), "algorithmic_flops": flops,
-            "kernel": kernel_name(cfg), "kernel_ms": round(k_avg, 4),
+            "kernel": "staged_gemm_kernel" if ran_staged else kernel_name(cfg),
+            "kernel_ms": round(k_avg, 4),
             "kernel_ms_median": round(k_med, 4), "kernel_ms_min": round(k_min, 4),
             "kernel_ms_p90": round(k_p90, 4),
             "alignment_ms": round(a_ms / max(a_n, 1), 4),
             "tile_staging_ms": round(g_ms / max(g_n, 1), 4),
             "algorithmic_bytes": bytes_alg,
-            "hbm_GBps_algorithmic": round(bytes_alg / (k_avg * 1e-3) / 1e9, 1)}
+            "hbm_GBps_algorithmic": round(bytes_alg / (k_avg * 1e-3) / 1e9, 1),
+            "path": "staged" if ran_staged else "fused"}
+    if ran_staged:  # the build kernel is part of the transfer: the path's own fraction too
+        path_ms = k_avg + b_avg
+        roof["staged_build_ms"] = round(b_avg, 4)
+        roof["transfer_kernels_ms"] = round(path_ms, 4)
+        roof["transfer_kernels_frac"] = round(flops / (path_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
     cpu = None
     if args.cpu_baseline_full:
         log("[bench] timing the CPU oracle over the whole step at full length")

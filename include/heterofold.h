@@ -256,6 +256,27 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
                                    const hf_rope* rope);
 
 /*
+ * Workspace bytes for the staged path of hf_transfer_kv (n_taps = 0) or
+ * hf_transfer_kv_taps (n_taps = 1..3): hf_transfer_workspace_bytes() plus a
+ * 16 KB table and one slab of aligned features per (role, receiver layer) for
+ * the interpolating map, or per (role, sender layer) for concatenated taps,
+ * each slab 2 bytes x 1024 features x the batch's receiver rows rounded up to
+ * 256 per sequence (about 61 MB per slab for one 29K-row sequence).  0 where
+ * the staged path does not apply: it serves bf16 with 8 sender and 8 receiver
+ * heads of d_h = 128.
+ * The transfer calls take the staged path when their workspace holds at least
+ * this many bytes, the shape is served, opts->k_norm is NULL, and (for
+ * concatenated taps, whose slabs several receiver layers share) opts->inv_r is
+ * NULL; otherwise the fused path.  Both compute the same values up to the
+ * order of the fp32 accumulation: the staged path builds x_j exactly as the
+ * fused path does (one bf16 rounding), stores it, and multiplies it in a
+ * separate kernel.  hf_transfer_kv_noalloc always takes the fused path.
+ */
+size_t hf_transfer_staged_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                                          const hf_kv_desc* sender, const hf_kv_desc* receiver,
+                                          const hf_rope* rope, int32_t n_taps);
+
+/*
  * Map the sender caches of B sequences to receiver caches.  For receiver
  * layer l, role c and receiver token j of sequence b:
  *   m_i = a_lo S[lo_l, c, :, i, :] + a_hi S[hi_l, c, :, i, :]      (layer map)
@@ -280,7 +301,9 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  *   bias           device fp32 [L_r][2][d_r], or NULL for zero bias.
  *   rope           NULL = no RoPE.
  *   opts           NULL, or the optional 1/r and key normalization (above).
- *   workspace      device, >= hf_transfer_workspace_bytes(), 256-B aligned.
+ *   workspace      device, >= hf_transfer_workspace_bytes(), 256-B aligned;
+ *                  >= hf_transfer_staged_workspace_bytes(..., 0) selects the
+ *                  staged path where it applies (see there).
  * Numerics: HF_F32 computes in fp32 throughout.  HF_BF16 forms x_j in fp32,
  * rounds it once to bf16 (round-to-nearest-even), multiplies on the matrix
  * cores with fp32 accumulation, adds bias and rotates in fp32, and rounds the
@@ -480,7 +503,9 @@ typedef enum {
   HF_KERNEL_RECOLOR_SOLVE = 6, /* all launches of hf_recolor_solve */
   HF_KERNEL_FOLD = 7,          /* all launches of hf_fold_map */
   HF_KERNEL_TRANSFER_STAGE = 8,/* per-tile alignment staging of hf_transfer_kv (bf16, tiled) */
-  HF_KERNEL_COUNT = 9
+  HF_KERNEL_STAGED_BUILD = 9,  /* staged path: aligned features of every slab to the workspace */
+  HF_KERNEL_STAGED_GEMM = 10,  /* staged path: the map products with bias and RoPE */
+  HF_KERNEL_COUNT = 11
 } hf_kernel_id;
 
 /*

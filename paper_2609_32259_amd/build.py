@@ -25,7 +25,7 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
-HIP_SOURCES = ["align.hip", "transfer.hip", "recolor.hip"]
+HIP_SOURCES = ["align.hip", "transfer.hip", "staged.hip", "recolor.hip"]
 HOST_SOURCES = ["abi.cpp"]
 
 # Packed fp32 VALU instructions are disabled for all device code.

@@ -387,6 +387,37 @@ size_t record_bytes(int32_t B, const int32_t* r_len, const hf_kv_desc* sender,
 
 }  // namespace
 
+namespace {
+
+// Staged path: 256-row tiles of the batch and the workspace it adds to the
+// fused path's (the RoPE table of positions 0..31, then the slabs).
+int64_t staged_row_tiles(int32_t B, const int32_t* r_len) {
+  int64_t n = 0;
+  for (int b = 0; b < B; ++b) n += r_len[b] > 0 ? ((int64_t)r_len[b] + hf::kStagedRows - 1) / hf::kStagedRows : 0;
+  return n;
+}
+size_t staged_extra_bytes(int32_t B, const int32_t* r_len, int n_slab_layers) {
+  return hf::kStagedT1Bytes +
+         (size_t)2 * n_slab_layers * (size_t)staged_row_tiles(B, r_len) * hf::kStagedRows * 1024 * 2;
+}
+
+}  // namespace
+
+size_t hf_transfer_staged_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
+                                          const hf_kv_desc* sender, const hf_kv_desc* receiver,
+                                          const hf_rope* rope, int32_t n_taps) {
+  if (B < 1 || B > HF_MAX_BATCH || !s_len || !r_len || !sender || !receiver) return 0;
+  if (n_taps < 0 || n_taps > 3) return 0;
+  if (!hf::staged_supported(sender->dtype, sender->H, receiver->H, sender->d_h) ||
+      receiver->d_h != sender->d_h)
+    return 0;
+  for (int b = 0; b < B; ++b)
+    if (s_len[b] < 0 || r_len[b] < 0) return 0;
+  const size_t base = hf_transfer_workspace_bytes(B, s_len, r_len, sender, receiver, rope);
+  if (base == 0) return 0;
+  return base + staged_extra_bytes(B, r_len, n_taps == 0 ? receiver->L : sender->L);
+}
+
 size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
                                    const hf_kv_desc* sender, const hf_kv_desc* receiver,
                                    const hf_rope* rope) {
@@ -506,6 +537,16 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
                 "this transfer needs %zu bytes of scratch, more than the %d bytes "
                 "hf_transfer_kv_noalloc holds; use hf_transfer_kv with a workspace",
                 ws_need, HF_NOALLOC_SCRATCH_BYTES);
+  // The staged path, where it applies and the workspace holds its slabs.
+  bool staged = false;
+  size_t st_need = 0;
+  if (!noalloc && hf::staged_supported(dtype, sender->H, receiver->H, d_h) && ws_need > 0 &&
+      !(opts && opts->k_norm) && !(ls.concat && opts && opts->inv_r)) {
+    st_need = ws_need + staged_extra_bytes(B, r_len, ls.concat ? L_s : L_r);
+    staged = workspace_bytes >= st_need;
+    for (int b = 0; staged && b < B; ++b)  // receiver rows are addressed with 32-bit byte offsets
+      if ((int64_t)r_len[b] * receiver->stride_t * 2 + 256 >= ((int64_t)1 << 31)) staged = false;
+  }
   if (ws_need > 0 && !noalloc) {
     if (!workspace) return fail(HF_ERR_NULL, "workspace is NULL");
     if (workspace_bytes < ws_need)
@@ -595,6 +636,19 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
     a.tile_rec = reinterpret_cast<const int32_t*>(w + rec_off);
     a.work_ctr = reinterpret_cast<int32_t*>(w + ws_need - 256);
   }
+  if (staged) {
+    a.cs_t1 = reinterpret_cast<const float*>(w + ws_need);
+    a.xs = reinterpret_cast<uint16_t*>(w + ws_need + hf::kStagedT1Bytes);
+    a.n_slab_layers = ls.concat ? L_s : L_r;
+    int rt = 0;
+    for (int b = 0; b < B; ++b) {
+      a.rt_start[b] = rt;
+      rt += (r_len[b] + hf::kStagedRows - 1) / hf::kStagedRows;
+    }
+    a.rt_start[B] = rt;
+    a.n_rt = rt;
+    a.xs_slab = (long long)rt * hf::kStagedRows * 1024;
+  }
   if (tiles == 0) return ok();
   if (a.tile_rec) {
     int dev = 0, n_cu = 0;
@@ -609,6 +663,8 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
     if (a.unrot) e = hf::launch_rope_table(const_cast<float*>(a.cs_s), rs.P_s, d_h, rope->theta_s, s);
     if (e == hipSuccess && a.rot)
       e = hf::launch_rope_table(const_cast<float*>(a.cs_r), rs.P_r, d_h, rope->theta_r, s);
+    if (e == hipSuccess && a.rot && staged)  // positions 0..31 for the staged epilogue
+      e = hf::launch_rope_table(const_cast<float*>(a.cs_t1), 32, d_h, rope->theta_r, s);
   }
   if (e != hipSuccess) return hip_fail(e, "RoPE table launch");
   if (a.tile_rec) {
@@ -616,6 +672,19 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
     e = hf::launch_transfer_stage(dtype, a, s);
   }
   if (e != hipSuccess) return hip_fail(e, "tile staging launch");
+  if (staged) {
+    {
+      TimedLaunch t(HF_KERNEL_STAGED_BUILD, s, timed);
+      e = hf::launch_staged_build(a, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "staged build launch");
+    {
+      TimedLaunch t(HF_KERNEL_STAGED_GEMM, s, timed);
+      e = hf::launch_staged_gemm(a, s);
+    }
+    if (e != hipSuccess) return hip_fail(e, "staged multiply launch");
+    return ok();
+  }
   {
     TimedLaunch t(HF_KERNEL_TRANSFER, s, timed);
     e = hf::launch_transfer(dtype, a, s);

@@ -81,7 +81,26 @@ struct TransferArgs {
   uint8_t taps[HF_MAX_LAYERS][3];
   float wlo[HF_MAX_LAYERS];
   float whi[HF_MAX_LAYERS];
+  // Staged path (bf16, 8 sender and 8 receiver heads of 128): the build writes
+  // the aligned features of every slab -- (role, receiver layer) for the
+  // interpolating map, (role, sender layer) for concatenated taps -- into xs,
+  // and the GEMM reads them back.  Slab layout: [256-row tile][32-feature
+  // k-tile][256 rows][32] bf16, sequences padded to whole 256-row tiles.
+  uint16_t* xs;            // nullptr: fused path
+  long long xs_slab;       // elements per slab
+  int32_t n_slab_layers;   // L_r (interpolating map) or sender layers (taps)
+  int32_t n_rt;            // 256-row tiles of the batch
+  int32_t rt_start[HF_MAX_BATCH + 1];  // first 256-row tile of each sequence
+  const float* cs_t1;      // receiver RoPE rows of positions 0..31 (cos | sin)
 };
+static_assert(sizeof(TransferArgs) <= 4096, "kernel argument size");
+
+// Staged path: the shapes it serves, its slab and table bytes, and its launches.
+bool staged_supported(int dtype, int H_s, int H_r, int d_h);
+constexpr int kStagedRows = 256;   // rows per GEMM tile
+constexpr size_t kStagedT1Bytes = 32 * 128 * 4;
+hipError_t launch_staged_build(const TransferArgs& a, hipStream_t s);
+hipError_t launch_staged_gemm(const TransferArgs& a, hipStream_t s);
 
 // Rows per workgroup tile of the transfer kernels.
 int transfer_rows_per_tile(int dtype, int H_r, int H_s, int n_taps, int d_h);

@@ -417,10 +417,18 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, int off) {
   return make_uint4(v[0], v[1], v[2], v[3]);
 }
 
-template <bool TWO_TAP, bool UNROT, int R>
+// Where a built X row goes: sink(r, f, v) stores features f..f+7 of tile row r.
+struct LdsSink {  // the X tile in LDS (row stride kXF)
+  uint16_t* Xs;
+  __device__ __forceinline__ void operator()(int r, int f, uint4 v) const {
+    *reinterpret_cast<uint4*>(Xs + r * kXF + f) = v;
+  }
+};
+
+template <bool TWO_TAP, bool UNROT, int R, class Sink>
 __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& p, const GroupLds& L,
                                              int base, int head, int r_first, int rpg, int lane,
-                                             uint16_t* Xs) {
+                                             const Sink& sink) {
   const int e0 = (lane & 7) * 8;
   const int kb = L.estart[r_first] - L.e_base;
   const int E = L.estart[r_first + rpg] - L.e_base - kb;
@@ -430,9 +438,8 @@ __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& 
   for (int q = 0; q < rpg; ++q) {  // rows without entries stay zero
     const int r = r_first + q;
     if (L.estart[r + 1] == L.estart[r]) {
-      uint16_t* xr = Xs + r * kXF + head * kDH;
-      *reinterpret_cast<uint4*>(xr + e0) = make_uint4(0, 0, 0, 0);
-      *reinterpret_cast<uint4*>(xr + 64 + e0) = make_uint4(0, 0, 0, 0);
+      sink(r, head * kDH + e0, make_uint4(0, 0, 0, 0));
+      sink(r, head * kDH + 64 + e0, make_uint4(0, 0, 0, 0));
     }
   }
   float rc[8], rs[8];  // U(p_base): closes every row of the group
@@ -515,9 +522,8 @@ __device__ __forceinline__ void build_groups(const Ctx& cx, const TransferArgs& 
           x[u + 8] = fmaf(b, rc[u], -a * rs[u]);
         }
       }
-      uint16_t* xr = Xs + (t.code & 63) * kXF + head * kDH;
-      *reinterpret_cast<uint4*>(xr + e0) = pack8(x);
-      *reinterpret_cast<uint4*>(xr + 64 + e0) = pack8(x + 8);
+      sink(t.code & 63, head * kDH + e0, pack8(x));
+      sink(t.code & 63, head * kDH + 64 + e0, pack8(x + 8));
 #pragma unroll
       for (int u = 0; u < 16; ++u) x[u] = 0.0f;
     }
@@ -710,6 +716,7 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
     const Ctx ct = make_ctx(p, it, tap);
     // ---- build X[64][d_in] of this tap ----
     if (staged) {
+      const LdsSink xsink{Xs};
       const int sh = wave / WPH;  // sender head this wave builds
       if (sh < H) {
         const GroupLds L{estart, ecol, ew, einfo, dt, e_base};
@@ -719,18 +726,18 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
         const int base = gbase[grp];
         if (MULTI) {  // one sender layer per tap
           if (tap == 0) {
-            if (unrot) build_groups<false, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
-            else build_groups<false, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+            if (unrot) build_groups<false, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, xsink);
+            else build_groups<false, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, xsink);
           } else {
-            if (unrot) build_groups<false, true, 2>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
-            else build_groups<false, false, 2>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+            if (unrot) build_groups<false, true, 2>(ct, p, L, base, sh, r_first, rpg, lane, xsink);
+            else build_groups<false, false, 2>(ct, p, L, base, sh, r_first, rpg, lane, xsink);
           }
         } else if (ct.two_tap) {
-          if (unrot) build_groups<true, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
-          else build_groups<true, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+          if (unrot) build_groups<true, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, xsink);
+          else build_groups<true, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, xsink);
         } else {
-          if (unrot) build_groups<false, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
-          else build_groups<false, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, Xs);
+          if (unrot) build_groups<false, true, 3>(ct, p, L, base, sh, r_first, rpg, lane, xsink);
+          else build_groups<false, false, 3>(ct, p, L, base, sh, r_first, rpg, lane, xsink);
         }
       }
     } else {
@@ -920,6 +927,98 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
   if (!kPersist || next >= n_items) break;
   __syncthreads();  // every wave is done with the staging rows; the next build writes X
   item = next;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Staged path, build: the aligned features of one (slab, 64-row tile) written
+// to global memory in the layout the staged GEMM reads.  A slab is (role,
+// receiver layer) for the interpolating map -- x_j of Sec. 3.1 with the layer
+// weights of its two taps -- or (role, sender layer) for concatenated taps --
+// one block x_j^t of Eq. 2, shared by every receiver layer that reads that
+// sender layer.  The arithmetic is the fused kernel's build (same staging
+// record, same group walk, one bf16 rounding per feature).
+// ---------------------------------------------------------------------------
+struct TiledSink {  // rows of one 64-row tile inside a slab's [256-row tile][k-tile][256][32]
+  uint16_t* tile;   // slab + 256-row tile base
+  int row0;         // the 64-row tile's first row inside its 256-row tile
+  __device__ __forceinline__ void operator()(int r, int f, uint4 v) const {
+    *reinterpret_cast<uint4*>(tile + (f >> 5) * (kStagedRows * 32) + (row0 + r) * 32 + (f & 31)) = v;
+  }
+};
+
+__global__ __launch_bounds__(512) void staged_build_kernel(const TransferArgs p) {
+  __shared__ __attribute__((aligned(16))) int ent[kRecBytes / 4];
+  __shared__ __attribute__((aligned(16))) float dt[kDMax * kDH];
+  int* estart = ent;
+  int* gbase = estart + 65;
+  int* ecol = gbase + 64;
+  float* ew = reinterpret_cast<float*>(ecol + kEMax);
+  int* einfo = reinterpret_cast<int*>(ew + kEMax);
+  const int* flag = einfo + kEMax;
+  const int* gstart = flag + 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  const int slab = blockIdx.x / p.tiles_per_lc;  // (role, layer), role-major
+  const int t = blockIdx.x - slab * p.tiles_per_lc;
+  Item it;
+  it.c = slab / p.n_slab_layers;
+  it.l = slab - it.c * p.n_slab_layers;
+  int b = 0;
+  while (b + 1 < p.B && p.tile_start[b + 1] <= t) ++b;
+  it.b = b;
+  it.tile = t - p.tile_start[b];
+  Ctx cx;
+  if (p.concat) {  // one sender layer, weight 1
+    const uint16_t* Sb = static_cast<const uint16_t*>(p.S) + it.b * p.s_sb + it.c * p.s_sc;
+    cx.S_lo = cx.S_hi = Sb + (long long)it.l * p.s_sl;
+    cx.cs_s = (it.c == 0 && p.unrot) ? p.cs_s + (long long)p.pos0_s[it.b] * kDH : nullptr;
+    cx.wlo = 1.0f;
+    cx.whi = 0.0f;
+    cx.two_tap = false;
+    cx.Ts = p.Ts[it.b];
+  } else {
+    cx = make_ctx(p, it);
+  }
+  // Keys un-rotate at the sender positions when the call asks for it; values
+  // never do (their context carries no sender table).
+  const bool unrot = cx.cs_s != nullptr;
+  copy16_to_lds(p.tile_rec + (long long)t * (kRecBytes / 4) + wave * 256 + 4 * lane, estart + wave * 256);
+  if (unrot) {  // U(0..15): rows 0..15 of the sender table, 2 per wave
+    const int ri = wave * 2 + (lane >> 5);
+    const int c = (lane & 31) ^ (ri & 1);
+    copy16_to_lds(p.cs_s + (long long)ri * kDH + 4 * c, dt + wave * 2 * kDH);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  const int Tr = p.Tr[it.b];
+  const int j0 = it.tile * 64;
+  const int nrows = min(64, Tr - j0);
+  const int g0 = p.row0[it.b] + j0;
+  const int rt = p.rt_start[it.b] + (it.tile >> 2);
+  const TiledSink sink{p.xs + slab * p.xs_slab + (long long)rt * (kStagedRows * kHMax * kDH),
+                       (it.tile & 3) * 64};
+  const bool staged = p.s_extent > 0 && flag[1] == 0 && !(unrot && flag[0] != 0);
+  if (staged) {  // eight sender heads: wave w builds head w
+    const GroupLds L{estart, ecol, ew, einfo, dt, estart[0]};
+    const int grp = lane >> 3;
+    const int r_first = gstart[grp], rpg = gstart[grp + 1] - r_first, base = gbase[grp];
+    if (cx.two_tap && unrot) build_groups<true, true, 3>(cx, p, L, base, wave, r_first, rpg, lane, sink);
+    else if (cx.two_tap) build_groups<true, false, 3>(cx, p, L, base, wave, r_first, rpg, lane, sink);
+    else if (unrot) build_groups<false, true, 3>(cx, p, L, base, wave, r_first, rpg, lane, sink);
+    else build_groups<false, false, 3>(cx, p, L, base, wave, r_first, rpg, lane, sink);
+  } else {
+    const int r = tid >> 3;        // 8 threads per row
+    const int e0 = (tid & 7) * 8;  // features e0..e0+7 and e0+64..e0+71 of every head
+    for (int h = 0; h < kHMax; ++h) {
+      float x[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) x[u] = 0.0f;
+      if (r < nrows) build_row_global(p, cx, g0 + r, h, e0, x);
+      sink(r, h * kDH + e0, pack8(x));
+      sink(r, h * kDH + 64 + e0, pack8(x + 8));
+    }
   }
 }
 
@@ -1224,6 +1323,19 @@ hipError_t noalloc_scratch(void** ptr) {
   }
   *ptr = per_device[dev];
   return hipSuccess;
+}
+
+bool staged_supported(int dtype, int H_s, int H_r, int d_h) {
+  return dtype == HF_BF16 && d_h == kDH && H_s == kHMax && H_r == kHMax;
+}
+
+hipError_t launch_staged_build(const TransferArgs& a, hipStream_t s) {
+  const long long items = (long long)a.tiles_per_lc * a.n_slab_layers * 2;
+  if (items <= 0) return hipSuccess;
+  if (!a.xs || !a.tile_rec || items > INT32_MAX) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)items);
+  hipLaunchKernelGGL(staged_build_kernel, grid, dim3(512), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_transfer(int dtype, const TransferArgs& a, hipStream_t s) {

@@ -33,6 +33,7 @@ HF_F32, HF_BF16 = 0, 1
 HF_KERNEL_TRANSFER, HF_KERNEL_ROPE_TABLES, HF_KERNEL_ALIGNMENT, HF_KERNEL_PACK = 0, 1, 2, 3
 HF_KERNEL_MOMENTS_STATS, HF_KERNEL_MOMENTS_COV, HF_KERNEL_RECOLOR_SOLVE, HF_KERNEL_FOLD = 4, 5, 6, 7
 HF_KERNEL_TRANSFER_STAGE = 8
+HF_KERNEL_STAGED_BUILD, HF_KERNEL_STAGED_GEMM = 9, 10
 HF_MAX_BATCH = 64
 ALIGN_MODES = {"overlap": HF_ALIGN_OVERLAP, "ta": HF_ALIGN_TA}
 
@@ -84,6 +85,9 @@ _SIGNATURES = {
                                  C.c_void_p, C.c_void_p]),
     "hf_transfer_workspace_bytes": (C.c_size_t, [C.c_int32, _I32P, _I32P, C.POINTER(hf_kv_desc),
                                                  C.POINTER(hf_kv_desc), C.POINTER(hf_rope)]),
+    "hf_transfer_staged_workspace_bytes": (C.c_size_t, [C.c_int32, _I32P, _I32P,
+                                                        C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc),
+                                                        C.POINTER(hf_rope), C.c_int32]),
     "hf_transfer_kv": (C.c_int32, [C.c_int32, _I32P, _I32P, C.c_void_p, C.c_void_p, C.c_void_p,
                                    C.c_void_p, _I32P, _I32P, _I32P, _I32P,
                                    C.POINTER(hf_kv_desc), C.POINTER(hf_kv_desc), C.c_void_p,
@@ -374,6 +378,18 @@ def hf_transfer_workspace_bytes(s_len, r_len, S, R, rope=None) -> int:
     return int(lib().hf_transfer_workspace_bytes(s_len.size, _p32(s_len), _p32(r_len),
                                                  C.byref(sd), C.byref(rd),
                                                  C.byref(rs) if rs is not None else None))
+
+
+def hf_transfer_staged_workspace_bytes(s_len, r_len, S, R, rope=None, n_taps=0) -> int:
+    """Workspace bytes that select the staged path (n_taps 0: hf_transfer_kv;
+    1..3: hf_transfer_kv_taps); 0 where it does not apply."""
+    s_len, r_len = _i32(s_len), _i32(r_len)
+    sd, rd = kv_desc(S), kv_desc(R)
+    rs, keep = _rope_struct(rope)
+    return int(lib().hf_transfer_staged_workspace_bytes(s_len.size, _p32(s_len), _p32(r_len),
+                                                        C.byref(sd), C.byref(rd),
+                                                        C.byref(rs) if rs is not None else None,
+                                                        int(n_taps)))
 
 
 def hf_transfer_kv(s_len, r_len, alignment: Alignment, layer_map, S, R, A_packed, bias=None,

@@ -26,10 +26,10 @@ def torch():
     return torch
 
 
-def _run(torch, cfg, wl, mode, taps, R=None):
+def _run(torch, cfg, wl, mode, taps, R=None, staged=None):
     from paper_2609_32259_amd.path import TransferPath
     path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r, mode=mode, R=R,
-                        layer_map="neighbor3")
+                        layer_map="neighbor3", staged=staged)
     path.build_alignment()
     if taps is None:
         path.build_layer_map()
@@ -40,11 +40,11 @@ def _run(torch, cfg, wl, mode, taps, R=None):
     return path
 
 
-def _compare_full(torch, cfg, wl, mode="overlap", taps=None):
+def _compare_full(torch, cfg, wl, mode="overlap", taps=None, staged=None):
     taps_np = lm.neighbor3(cfg.L_s, cfg.L_r) if taps is None else np.asarray(taps)
     print(f"[gpu-taps] {cfg.name} mode={mode} B={wl.seg.batch} T_r={list(wl.seg.r_len)} "
-          f"n_taps={taps_np.shape[1]} rope={wl.rope is not None}", flush=True)
-    path = _run(torch, cfg, wl, mode, taps)
+          f"n_taps={taps_np.shape[1]} rope={wl.rope is not None} staged={staged}", flush=True)
+    path = _run(torch, cfg, wl, mode, taps, staged=staged)
     Case(cfg, wl, path.R, mode, layer_map=taps_np, tag="gpu-taps").check_all()
 
 
@@ -55,11 +55,18 @@ def test_taps_fp32(torch, mode):
     _compare_full(torch, cfg, wl, mode)
 
 
-def test_taps_bf16_14b_shape_small(torch):
+# The staged path (aligned features of each sender layer written to the
+# workspace, then a separate multiply) serves bf16 with 8 sender and 8 receiver
+# heads and is the default there; tests of that shape run both paths.
+BOTH_PATHS = pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
+
+
+@BOTH_PATHS
+def test_taps_bf16_14b_shape_small(torch, staged):
     cfg = synth.LLAMA8B_14B_8K.with_(name="14b n3 small", layer_map="neighbor3", T_s=300, L_r=6)
     wl = synth.make_workload(cfg, seed=21, device="cuda")
-    _compare_full(torch, cfg, wl, "overlap")
-    _compare_full(torch, cfg, wl, "ta")
+    _compare_full(torch, cfg, wl, "overlap", staged=staged)
+    _compare_full(torch, cfg, wl, "ta", staged=staged)
 
 
 def test_taps_bf16_four_receiver_heads_outlier_keys(torch):
@@ -92,8 +99,9 @@ def test_taps_bf16_reverse_batched(torch):
     _compare_full(torch, cfg, synth.Workload(cfg, seg, S, A, bias, rope), "overlap")
 
 
+@BOTH_PATHS
 @pytest.mark.parametrize("n_taps", [1, 2])
-def test_taps_bf16_other_tap_counts(torch, n_taps):
+def test_taps_bf16_other_tap_counts(torch, n_taps, staged):
     base = synth.LLAMA8B_14B_8K.with_(name=f"14b {n_taps} taps", T_s=200, L_r=4)
     cfg = base.with_(layer_map="neighbor3")
     seg = synth.make_segmentation(cfg, seed=25)
@@ -105,7 +113,7 @@ def test_taps_bf16_other_tap_counts(torch, n_taps):
     taps = np.array([[0, 31, 7][:n_taps], [5, 5, 5][:n_taps], [31, 0, 16][:n_taps],
                      [12, 13, 14][:n_taps]], np.int32)
     _compare_full(torch, cfg, synth.Workload(cfg, seg, S, A, bias, synth.rope_params(cfg)),
-                  "overlap", taps=taps)
+                  "overlap", taps=taps, staged=staged)
 
 
 def test_taps_bf16_beyond_staging_capacity(torch):
@@ -128,7 +136,8 @@ def test_taps_bf16_beyond_staging_capacity(torch):
                   "overlap")
 
 
-def test_taps_bf16_identity_first_block_is_bit_exact(torch):
+@BOTH_PATHS
+def test_taps_bf16_identity_first_block_is_bit_exact(torch, staged):
     cfg = synth.LLAMA8B_14B_8K.with_(name="n3 identity", layer_map="neighbor3", L_s=9, L_r=9,
                                      T_s=150, rope=None)
     wl = synth.make_workload(cfg, seed=27, device="cuda")
@@ -138,19 +147,20 @@ def test_taps_bf16_identity_first_block_is_bit_exact(torch):
     wl = synth.Workload(cfg, seg, wl.S, A, None, None)
     taps = lm.neighbor3(cfg.L_s, cfg.L_r)
     for mode in ("overlap", "ta"):
-        R = _run(torch, cfg, wl, mode, None).R
+        R = _run(torch, cfg, wl, mode, None, staged=staged).R
         for l in range(cfg.L_r):
             assert torch.equal(R[0, l, :, :, :150, :].view(torch.int16),
                                wl.S[0, int(taps[l, 0]), :, :, :150, :].view(torch.int16))
 
 
-def test_full_14b_shape_32k_neighbor3(torch):
-    """The benchmark's neighbourhood-map workload: every layer and role, on
-    windows of rows."""
+@BOTH_PATHS
+def test_full_14b_shape_32k_neighbor3(torch, staged):
+    """The benchmark's neighbourhood-map workload (the staged path is the
+    benchmark's): every layer and role, on windows of rows."""
     cfg = synth.LLAMA8B_14B_32K_N3
     wl = synth.make_workload(cfg, seed=0, device="cuda")
-    print(f"[gpu-taps] full-size {cfg.name} T_r={list(wl.seg.r_len)}", flush=True)
-    path = _run(torch, cfg, wl, "overlap", None)
+    print(f"[gpu-taps] full-size {cfg.name} T_r={list(wl.seg.r_len)} staged={staged}", flush=True)
+    path = _run(torch, cfg, wl, "overlap", None, staged=staged)
     rng = np.random.default_rng(98)
     Case(cfg, wl, path.R, tag="gpu-taps-32k").check_all(
         windows_of=lambda b, T_r: windows(T_r, 64, rng, n_mid=2, width=384))

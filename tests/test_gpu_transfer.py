@@ -27,23 +27,23 @@ def torch():
     return torch
 
 
-def _path(cfg, wl, mode="overlap", rope=None, R=None):
+def _path(cfg, wl, mode="overlap", rope=None, R=None, staged=None):
     from paper_2609_32259_amd.path import TransferPath
     return TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope if rope is None else rope,
-                        cfg.L_r, cfg.H_r, mode=mode, R=R)
+                        cfg.L_r, cfg.H_r, mode=mode, R=R, staged=staged)
 
 
 def _np64(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
-def _compare_full(torch, cfg, wl, mode="overlap", rope="cfg", R=None):
+def _compare_full(torch, cfg, wl, mode="overlap", rope="cfg", R=None, staged=None):
     """Every element of every layer, role and sequence."""
     if rope != "cfg":
         wl = synth.Workload(cfg, wl.seg, wl.S, wl.A, wl.bias, rope, wl.opts)
     print(f"[gpu-transfer] {cfg.name} mode={mode} B={wl.seg.batch} T_s={list(wl.seg.s_len)} "
-          f"T_r={list(wl.seg.r_len)} rope={wl.rope is not None}", flush=True)
-    path = _path(cfg, wl, mode, R=R)
+          f"T_r={list(wl.seg.r_len)} rope={wl.rope is not None} staged={staged}", flush=True)
+    path = _path(cfg, wl, mode, R=R, staged=staged)
     R = path.step()
     torch.cuda.synchronize()
     Case(cfg, wl, R, mode, tag="gpu-transfer").check_all()
@@ -70,11 +70,18 @@ def test_fp32_rope_batched_offsets(torch):
 
 # --- bf16, small sizes, every element ----------------------------------------
 
+# The staged path (aligned features written to the workspace, then a separate
+# multiply) serves bf16 with 8 sender and 8 receiver heads; tests of that shape
+# run both paths.
+BOTH_PATHS = pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
+
+
+@BOTH_PATHS
 @pytest.mark.parametrize("mode", ["overlap", "ta"])
-def test_bf16_14b_shape_small(torch, mode):
+def test_bf16_14b_shape_small(torch, mode, staged):
     cfg = synth.LLAMA8B_14B_8K.with_(T_s=300)          # 5 row tiles of 64, ragged tail
     wl = synth.make_workload(cfg, seed=2, device="cuda")
-    _compare_full(torch, cfg, wl, mode)
+    _compare_full(torch, cfg, wl, mode, staged=staged)
 
 
 def test_bf16_qwen7b_shape_small(torch):
@@ -100,8 +107,8 @@ def test_bf16_reverse_batched_ragged(torch):
     _compare_full(torch, cfg, wl, "overlap")
 
 
-@pytest.mark.parametrize("H_r", [8, 4])
-def test_bf16_batch_with_empty_sequences(torch, H_r):
+@pytest.mark.parametrize("H_r,staged", [(8, False), (8, True), (4, False)])
+def test_bf16_batch_with_empty_sequences(torch, H_r, staged):
     # A sequence with no tokens and one with sender tokens but no receiver
     # tokens own no row tiles (and no staging records); the sequences around
     # them still map correctly, and no receiver row outside the lengths changes.
@@ -123,7 +130,7 @@ def test_bf16_batch_with_empty_sequences(torch, H_r):
     T_cap = int(seg.r_len.max()) + 21
     R = torch.full((4, cfg.L_r, 2, cfg.H_r, T_cap, cfg.d_h), 3.0, dtype=torch.bfloat16,
                    device="cuda")
-    _compare_full(torch, cfg, wl, "overlap", R=R)
+    _compare_full(torch, cfg, wl, "overlap", R=R, staged=staged)
     for b in range(4):
         T_r = int(seg.r_len[b])
         assert bool((R[b, :, :, :, T_r:, :] == 3.0).all()), f"sequence {b}: rows past {T_r} changed"
@@ -153,8 +160,8 @@ def test_bf16_tiles_beyond_staging_capacity(torch, H_r):
     _compare_full(torch, cfg, wl, "overlap")
 
 
-@pytest.mark.parametrize("H_r", [8, 4])
-def test_bf16_full_batch_of_short_sequences(torch, H_r):
+@pytest.mark.parametrize("H_r,staged", [(8, False), (8, True), (4, False)])
+def test_bf16_full_batch_of_short_sequences(torch, H_r, staged):
     # 64 sequences (the batch limit) of 0 to 200 sender tokens: many tiles with
     # ragged tails, sequences without tiles, and fewer work items than compute
     # units at L_r = 1, so the work decoding and the per-sequence tile starts are
@@ -175,7 +182,7 @@ def test_bf16_full_batch_of_short_sequences(torch, H_r):
     T_cap = int(seg.r_len.max()) + 5
     R = torch.full((64, cfg.L_r, 2, cfg.H_r, T_cap, cfg.d_h), 3.0, dtype=torch.bfloat16,
                    device="cuda")
-    _compare_full(torch, cfg, wl, "overlap", R=R)
+    _compare_full(torch, cfg, wl, "overlap", R=R, staged=staged)
     for b in range(64):
         T_r = int(seg.r_len[b])
         assert bool((R[b, :, :, :, T_r:, :] == 3.0).all()), f"sequence {b}: rows past {T_r} changed"
@@ -267,13 +274,14 @@ def test_bf16_equal_rope_round_trip(torch):
     assert torch.equal(R[0, :, 1, :, :150, :].view(torch.int16), wl.S[0, :, 1, :, :150, :].view(torch.int16))
 
 
-def test_bf16_rows_past_length_untouched_and_deterministic(torch):
+@BOTH_PATHS
+def test_bf16_rows_past_length_untouched_and_deterministic(torch, staged):
     cfg = synth.LLAMA8B_14B_8K.with_(T_s=260, L_r=4)
     wl = synth.make_workload(cfg, seed=8, device="cuda")
     T_r = int(wl.seg.r_len[0])
     R = torch.full((1, cfg.L_r, 2, cfg.H_r, T_r + 37, cfg.d_h), 7.0, dtype=torch.bfloat16,
                    device="cuda")
-    path = _path(cfg, wl, R=R)
+    path = _path(cfg, wl, R=R, staged=staged)
     out1 = path.step().clone()
     out2 = path.step().clone()
     torch.cuda.synchronize()
@@ -296,11 +304,11 @@ def test_bf16_sender_head_counts(torch, H_s, H_r):
 
 # --- bf16, full sizes ----------------------------------------------------------
 
-def _run_full(torch, cfg, seed=0):
+def _run_full(torch, cfg, seed=0, staged=None):
     wl = synth.make_workload(cfg, seed=seed, device="cuda")
     print(f"[gpu-transfer] full-size {cfg.name} B={wl.seg.batch} T_s={list(wl.seg.s_len)} "
-          f"T_r={list(wl.seg.r_len)}", flush=True)
-    R = _path(cfg, wl).step()
+          f"T_r={list(wl.seg.r_len)} staged={staged}", flush=True)
+    R = _path(cfg, wl, staged=staged).step()
     torch.cuda.synchronize()
     return wl, R
 
@@ -327,12 +335,13 @@ def test_full_reverse_batch4(torch, T):
     _compare_windows(torch, synth.QWEN7B_LLAMA8B_B4.with_(T_s=T), width=512, n_mid=2)
 
 
-@pytest.fixture(scope="module")
-def full_32k(torch):
-    """The headline workload, run once in the benchmark's launch configuration."""
+@pytest.fixture(scope="module", params=[False, True], ids=["fused", "staged"])
+def full_32k(torch, request):
+    """The headline workload, run once per path in the benchmark's launch
+    configuration (the fused path is the benchmark's)."""
     cfg = synth.LLAMA8B_14B_32K
-    wl, R = _run_full(torch, cfg)
-    yield Case(cfg, wl, R, tag="gpu-transfer-32k")
+    wl, R = _run_full(torch, cfg, staged=request.param)
+    yield Case(cfg, wl, R, tag=f"gpu-transfer-32k-{'staged' if request.param else 'fused'}")
     del wl, R
     torch.cuda.empty_cache()
 
