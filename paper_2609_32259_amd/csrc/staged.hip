@@ -143,23 +143,29 @@ FI void rd_frags(const Lane& L, const unsigned char* sb, int ks, bf16x8 (&fx)[kM
 #pragma unroll
   for (int q = 0; q < 4; ++q) fw[q] = *reinterpret_cast<const bf16x8*>(sb + ks * 8192 + L.wo + q * 1024);
 }
+// ZERO: the first k-step of a work item, which starts the accumulators from 0.
+template <bool ZERO>
 FI void mfma4(f32x16 (&acc)[kMB][4], const bf16x8 (&fx)[kMB], const bf16x8 (&fw)[4], int m) {
+  const f32x16 zero = {};
 #pragma unroll
   for (int q = 0; q < 4; ++q)
-    acc[m][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[q], fx[m], acc[m][q], 0, 0, 0);
+    acc[m][q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[q], fx[m], ZERO ? zero : acc[m][q], 0, 0, 0);
 }
 
 // One k-tile.  f0x/f0w hold its k-step-0 fragments (read during the previous
 // k-tile); sb is its stage, sn the next k-tile's, sd the stage that k-tile kd
 // of job D (this job's k-tile kt + 3, or the next job's first ones) is loaded
-// into.  WAIT: wait for this wave's loads of k-tile kt + 1 (all but the 4 of
-// k-tile kt + 2 issued after them); the first two k-tiles of a job find theirs
-// landed already.  The issue order is fixed: fragments for k-step 1, then each
-// group of 4 MFMAs after one stage load.
-template <bool WAIT>
+// into.  The wait lets at most NV vector-memory operations of this wave stay
+// outstanding, so that its loads of k-tile kt + 1 have landed: in steady state
+// only the 4 loads of k-tile kt + 2 were issued after them; in the first two
+// k-tiles of a work item the previous item's 16 receiver-row stores (and the
+// bias and RoPE-row loads of waves 0..3) were issued after them too.  FIRST:
+// k-tile 0 of a work item.  The issue order is fixed: fragments for k-step 1,
+// then each group of 4 MFMAs after one stage load.
+template <int NV, bool FIRST>
 FI void ktile(const Lane& L, f32x16 (&acc)[kMB][4], bf16x8 (&f0x)[kMB], bf16x8 (&f0w)[4], bool more,
               unsigned char* sb, unsigned char* sn, unsigned char* sd, const Job& D, int wbytes, int kd) {
-  if (WAIT) __builtin_amdgcn_s_waitcnt(wait_vm(4));
+  __builtin_amdgcn_s_waitcnt(wait_vm(NV));
   __builtin_amdgcn_s_barrier();  // ... for every wave; stage sd is no longer read
   SB();
   bf16x8 f1x[kMB], f1w[4];
@@ -169,7 +175,7 @@ FI void ktile(const Lane& L, f32x16 (&acc)[kMB][4], bf16x8 (&f0x)[kMB], bf16x8 (
 #pragma unroll
   for (int m = 0; m < kMB; ++m) {
     dma_w(L, D.wb, wbytes, D.nt, kd, sd, m);
-    mfma4(acc, f0x, f0w, m);
+    mfma4<FIRST>(acc, f0x, f0w, m);
     SB();
   }
   if (more) rd_frags(L, sn, 0, f0x, f0w);
@@ -177,7 +183,7 @@ FI void ktile(const Lane& L, f32x16 (&acc)[kMB][4], bf16x8 (&f0x)[kMB], bf16x8 (
 #pragma unroll
   for (int m = 0; m < kMB; ++m) {
     dma_x(L, xt, kd, sd, m);
-    mfma4(acc, f1x, f1w, m);
+    mfma4<false>(acc, f1x, f1w, m);
     SB();
   }
 }
@@ -202,7 +208,9 @@ FI void rope_cs(const Lane& L, const float* st0row, const float* st1, int qq, in
 
 // One 32-row block of the wave's 64 x 128 tile: bias, receiver RoPE (ROT),
 // bf16, then two staged passes that each write 64 features of the 32 rows as
-// 128-byte row halves.
+// 128-byte row halves.  Staging row rr keeps its 16-byte chunk c at slot
+// c ^ ((rr >> 1) & 7): the 32 rows of one 8-byte write then cover 16 distinct
+// 16-byte bank groups, the most a 128-byte row stride allows.
 template <bool ROT, int m>
 FI void epi_block(const Lane& L, const f32x16 (&acc)[kMB][4], int j0, int Tr, long long r_st,
                   const float* bsh, uint16_t* stg, __amdgpu_buffer_rsrc_t rR, const float* st0,
@@ -247,13 +255,13 @@ FI void epi_block(const Lane& L, const f32x16 (&acc)[kMB][4], int j0, int Tr, lo
         const uint2 v = ph == 0 ? v0[qq][g]
                                 : make_uint2(pack2(keep[qq][g][0], keep[qq][g][1]),
                                              pack2(keep[qq][g][2], keep[qq][g][3]));
-        *reinterpret_cast<uint2*>(stg + rr * 64 + ((c ^ (rr & 7)) * 8) + (L.lane >> 5) * 4) = v;
+        *reinterpret_cast<uint2*>(stg + rr * 64 + ((c ^ ((rr >> 1) & 7)) * 8) + (L.lane >> 5) * 4) = v;
       }
 #pragma unroll
     for (int pp = 0; pp < 4; ++pp) {
       const int ch = L.lane + 64 * pp;
       const int r2 = ch >> 3, c = ch & 7;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r2 * 64 + ((c ^ (r2 & 7)) * 8));
+      const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r2 * 64 + ((c ^ ((r2 >> 1) & 7)) * 8));
       const int jj = j0 + 64 * L.wr + 32 * m + r2;
       const int off = jj < Tr ? (int)(jj * r_st * 2) + 128 * ph + c * 16 : (int)0x80000000;
       __builtin_amdgcn_raw_buffer_store_b128(v, rR, off, 0, 2);  // non-temporal: not read again here
@@ -331,13 +339,7 @@ __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs 
     }
   }
   __builtin_amdgcn_s_waitcnt(0);
-  f32x16 acc[kMB][4];
-#pragma unroll
-  for (int m = 0; m < kMB; ++m)
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[m][q][i] = 0.0f;
+  f32x16 acc[kMB][4];  // set by each work item's first k-step
   bf16x8 f0x[kMB], f0w[4];
   __builtin_amdgcn_s_barrier();
   rd_frags(L, s0, 0, f0x, f0w);
@@ -355,24 +357,27 @@ __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs 
       __builtin_amdgcn_global_load_lds(p.cs_r + (long long)(J.pos0 + jb) * 128 + (L.lane & 31) * 4,
                                        (lds_void_t*)(st0 + 2 * L.wave * 128), 16, 0, 0);
     }
-    // k-tiles 0..3 (their stages were filled before this job began)
-    ktile<false>(L, acc, f0x, f0w, true, s0, s1, s3, J, wbytes, 3);
-    ktile<false>(L, acc, f0x, f0w, true, s1, s2, s0, J, wbytes, 4);
-    ktile<true>(L, acc, f0x, f0w, true, s2, s3, s1, J, wbytes, 5);
-    ktile<true>(L, acc, f0x, f0w, true, s3, s0, s2, J, wbytes, 6);
+    // k-tiles 0..3 (k-tile 0 landed before the previous item's epilogue)
+    ktile<20, true>(L, acc, f0x, f0w, true, s0, s1, s3, J, wbytes, 3);
+    ktile<20, false>(L, acc, f0x, f0w, true, s1, s2, s0, J, wbytes, 4);
+    ktile<4, false>(L, acc, f0x, f0w, true, s2, s3, s1, J, wbytes, 5);
+    ktile<4, false>(L, acc, f0x, f0w, true, s3, s0, s2, J, wbytes, 6);
     for (int kt = 4; kt < KT - 4; kt += 4) {
-      ktile<true>(L, acc, f0x, f0w, true, s0, s1, s3, J, wbytes, kt + 3);
-      ktile<true>(L, acc, f0x, f0w, true, s1, s2, s0, J, wbytes, kt + 4);
-      ktile<true>(L, acc, f0x, f0w, true, s2, s3, s1, J, wbytes, kt + 5);
-      ktile<true>(L, acc, f0x, f0w, true, s3, s0, s2, J, wbytes, kt + 6);
+      ktile<4, false>(L, acc, f0x, f0w, true, s0, s1, s3, J, wbytes, kt + 3);
+      ktile<4, false>(L, acc, f0x, f0w, true, s1, s2, s0, J, wbytes, kt + 4);
+      ktile<4, false>(L, acc, f0x, f0w, true, s2, s3, s1, J, wbytes, kt + 5);
+      ktile<4, false>(L, acc, f0x, f0w, true, s3, s0, s2, J, wbytes, kt + 6);
     }
     // the last 4 k-tiles: this job's last one, then the next job's first three
-    ktile<true>(L, acc, f0x, f0w, true, s0, s1, s3, J, wbytes, KT - 1);
-    ktile<true>(L, acc, f0x, f0w, true, s1, s2, s0, N, wbytes, 0);
-    ktile<true>(L, acc, f0x, f0w, true, s2, s3, s1, N, wbytes, 1);
-    ktile<true>(L, acc, f0x, f0w, false, s3, s0, s2, N, wbytes, 2);
-    __builtin_amdgcn_s_waitcnt(0);  // the next job's k-tiles 0..2, this job's bias and RoPE rows
-    __builtin_amdgcn_s_barrier();   // ... for every wave
+    ktile<4, false>(L, acc, f0x, f0w, true, s0, s1, s3, J, wbytes, KT - 1);
+    ktile<4, false>(L, acc, f0x, f0w, true, s1, s2, s0, N, wbytes, 0);
+    ktile<4, false>(L, acc, f0x, f0w, true, s2, s3, s1, N, wbytes, 1);
+    ktile<4, false>(L, acc, f0x, f0w, false, s3, s0, s2, N, wbytes, 2);
+    // The wait at the start of the last k-tile left only the next job's k-tile
+    // 1 loads outstanding, so this job's bias and RoPE rows and the next job's
+    // k-tile 0 have landed; k-tiles 1 and 2 keep loading through the epilogue,
+    // into stages the epilogue does not touch.
+    __builtin_amdgcn_s_barrier();  // every wave is past its last read of stage 3
     if (has_next) dma_bias(N, (tloc + 1) & 1);
     {
       const __amdgpu_buffer_rsrc_t rR =
@@ -383,13 +388,7 @@ __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs 
       else epilogue<false>(L, acc, J.j0, J.Tr, p.r_st, bias_base, stg, rR, st0, st1);
     }
     if (!has_next) break;
-#pragma unroll
-    for (int m = 0; m < kMB; ++m)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[m][q][i] = 0.0f;
-    __builtin_amdgcn_s_barrier();  // staging in stage 3 is read; every wave's loads of k-tiles 0..2 landed
+    __builtin_amdgcn_s_barrier();  // staging in stage 3 is read
     rd_frags(L, s0, 0, f0x, f0w);
     jj = jn;
     J = N;
