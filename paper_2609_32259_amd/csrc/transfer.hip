@@ -932,22 +932,18 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
 
 // ---------------------------------------------------------------------------
 // Staged path, build: the aligned features of one (slab, 64-row tile) written
-// to global memory in the layout the staged GEMM reads.  A slab is (role,
+// to global memory in the layout the staged GEMM reads.  The tile is built in
+// LDS and then written out: in the slab's [256-row tile][k-tile][256][32]
+// layout its rows are one 4 KB run per k-tile, so every wave store is 1 KB of
+// whole lines (rows past the sequence end carry zeros the GEMM never stores).  A slab is (role,
 // receiver layer) for the interpolating map -- x_j of Sec. 3.1 with the layer
 // weights of its two taps -- or (role, sender layer) for concatenated taps --
 // one block x_j^t of Eq. 2, shared by every receiver layer that reads that
 // sender layer.  The arithmetic is the fused kernel's build (same staging
 // record, same group walk, one bf16 rounding per feature).
 // ---------------------------------------------------------------------------
-struct TiledSink {  // rows of one 64-row tile inside a slab's [256-row tile][k-tile][256][32]
-  uint16_t* tile;   // slab + 256-row tile base
-  int row0;         // the 64-row tile's first row inside its 256-row tile
-  __device__ __forceinline__ void operator()(int r, int f, uint4 v) const {
-    *reinterpret_cast<uint4*>(tile + (f >> 5) * (kStagedRows * 32) + (row0 + r) * 32 + (f & 31)) = v;
-  }
-};
-
 __global__ __launch_bounds__(512) void staged_build_kernel(const TransferArgs p) {
+  __shared__ __attribute__((aligned(16))) uint16_t xl[64 * kXF];  // the built tile, fused-kernel layout
   __shared__ __attribute__((aligned(16))) int ent[kRecBytes / 4];
   __shared__ __attribute__((aligned(16))) float dt[kDMax * kDH];
   int* estart = ent;
@@ -996,9 +992,10 @@ __global__ __launch_bounds__(512) void staged_build_kernel(const TransferArgs p)
   const int j0 = it.tile * 64;
   const int nrows = min(64, Tr - j0);
   const int g0 = p.row0[it.b] + j0;
+  const LdsSink sink{xl};
   const int rt = p.rt_start[it.b] + (it.tile >> 2);
-  const TiledSink sink{p.xs + slab * p.xs_slab + (long long)rt * (kStagedRows * kHMax * kDH),
-                       (it.tile & 3) * 64};
+  uint16_t* dst = p.xs + slab * p.xs_slab + (long long)rt * (kStagedRows * kHMax * kDH) +
+                  (it.tile & 3) * 64 * 32;
   const bool staged = p.s_extent > 0 && flag[1] == 0 && !(unrot && flag[0] != 0);
   if (staged) {  // eight sender heads: wave w builds head w
     const GroupLds L{estart, ecol, ew, einfo, dt, estart[0]};
@@ -1008,6 +1005,15 @@ __global__ __launch_bounds__(512) void staged_build_kernel(const TransferArgs p)
     else if (cx.two_tap) build_groups<true, false, 3>(cx, p, L, base, wave, r_first, rpg, lane, sink);
     else if (unrot) build_groups<false, true, 3>(cx, p, L, base, wave, r_first, rpg, lane, sink);
     else build_groups<false, false, 3>(cx, p, L, base, wave, r_first, rpg, lane, sink);
+    // The wave's own head (k-tiles 4 wave .. 4 wave + 3 of the 64 rows) goes
+    // out as soon as its walk ends: LDS operations of one wave run in order.
+    const int c8 = (lane & 3) * 8;
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+      const int kt = 4 * wave + (i >> 2), r = 16 * (i & 3) + (lane >> 2);
+      *reinterpret_cast<uint4*>(dst + kt * (kStagedRows * 32) + r * 32 + c8) =
+          *reinterpret_cast<const uint4*>(xl + r * kXF + kt * 32 + c8);
+    }
   } else {
     const int r = tid >> 3;        // 8 threads per row
     const int e0 = (tid & 7) * 8;  // features e0..e0+7 and e0+64..e0+71 of every head
@@ -1019,6 +1025,12 @@ __global__ __launch_bounds__(512) void staged_build_kernel(const TransferArgs p)
       sink(r, h * kDH + e0, pack8(x));
       sink(r, h * kDH + 64 + e0, pack8(x + 8));
     }
+    __syncthreads();
+    const int r2 = (tid & 255) >> 2, c8 = (tid & 3) * 8;
+#pragma unroll 4
+    for (int kt = tid >> 8; kt < kHMax * kDH / 32; kt += 2)
+      *reinterpret_cast<uint4*>(dst + kt * (kStagedRows * 32) + r2 * 32 + c8) =
+          *reinterpret_cast<const uint4*>(xl + r2 * kXF + kt * 32 + c8);
   }
 }
 
