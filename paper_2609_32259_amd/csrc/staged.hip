@@ -188,6 +188,29 @@ FI void ktile(const Lane& L, f32x16 (&acc)[kMB][4], bf16x8 (&f0x)[kMB], bf16x8 (
   }
 }
 
+// Staging accesses of the epilogue, written as instructions the compiler does
+// not see as LDS accesses.  Stage 3 was last filled by a load into LDS that the
+// explicit waits have completed, but the compiler cannot tell which load in
+// flight targets which stage and would wait for all of them, the next work
+// item's k-tiles included.  The four reads end with their own wait.
+FI uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+FI void stg_write8(uint32_t a, uint2 v) {
+  asm volatile("ds_write_b64 %0, %1" : : "v"(a), "v"(v) : "memory");
+}
+FI void stg_read4x16(const uint32_t (&a)[4], u32x4 (&v)[4]) {
+  asm volatile(
+      "ds_read_b128 %0, %4\n\t"
+      "ds_read_b128 %1, %5\n\t"
+      "ds_read_b128 %2, %6\n\t"
+      "ds_read_b128 %3, %7\n\t"
+      "s_waitcnt lgkmcnt(0)"
+      : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+      : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3])
+      : "memory");
+}
+
 // RoPE angles of the lane's row as a sum: the row's 32-row block base (st0 row)
 // plus its offset r < 32 in the block (st1 row r, stored with chunk c of row r
 // at slot c ^ r).  cos(a + b) = cos a cos b - sin a sin b, sin(a + b) = ...
@@ -255,13 +278,22 @@ FI void epi_block(const Lane& L, const f32x16 (&acc)[kMB][4], int j0, int Tr, lo
         const uint2 v = ph == 0 ? v0[qq][g]
                                 : make_uint2(pack2(keep[qq][g][0], keep[qq][g][1]),
                                              pack2(keep[qq][g][2], keep[qq][g][3]));
-        *reinterpret_cast<uint2*>(stg + rr * 64 + ((c ^ ((rr >> 1) & 7)) * 8) + (L.lane >> 5) * 4) = v;
+        stg_write8(lds_addr(stg + rr * 64 + ((c ^ ((rr >> 1) & 7)) * 8) + (L.lane >> 5) * 4), v);
       }
+    uint32_t ra[4];
+    u32x4 rv[4];
 #pragma unroll
     for (int pp = 0; pp < 4; ++pp) {
       const int ch = L.lane + 64 * pp;
       const int r2 = ch >> 3, c = ch & 7;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(stg + r2 * 64 + ((c ^ ((r2 >> 1) & 7)) * 8));
+      ra[pp] = lds_addr(stg + r2 * 64 + ((c ^ ((r2 >> 1) & 7)) * 8));
+    }
+    stg_read4x16(ra, rv);
+#pragma unroll
+    for (int pp = 0; pp < 4; ++pp) {
+      const int ch = L.lane + 64 * pp;
+      const int r2 = ch >> 3, c = ch & 7;
+      const u32x4 v = rv[pp];
       const int jj = j0 + 64 * L.wr + 32 * m + r2;
       const int off = jj < Tr ? (int)(jj * r_st * 2) + 128 * ph + c * 16 : (int)0x80000000;
       __builtin_amdgcn_raw_buffer_store_b128(v, rR, off, 0, 2);  // non-temporal: not read again here
@@ -378,7 +410,6 @@ __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs 
     // k-tile 0 have landed; k-tiles 1 and 2 keep loading through the epilogue,
     // into stages the epilogue does not touch.
     __builtin_amdgcn_s_barrier();  // every wave is past its last read of stage 3
-    if (has_next) dma_bias(N, (tloc + 1) & 1);
     {
       const __amdgpu_buffer_rsrc_t rR =
           mk_rsrc(J.rbase + (long long)L.wc * p.r_sh, (int)((long long)J.Tr * p.r_st * 2));
@@ -388,12 +419,17 @@ __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs 
       else epilogue<false>(L, acc, J.j0, J.Tr, p.r_st, bias_base, stg, rR, st0, st1);
     }
     if (!has_next) break;
+    // The next job's bias goes into the other half of sbias only now: a load
+    // into LDS issued before the epilogue's LDS reads would make them wait for
+    // every load in flight, the next job's k-tiles 1 and 2 included.
+    dma_bias(N, (tloc + 1) & 1);
     __builtin_amdgcn_s_barrier();  // staging in stage 3 is read
     rd_frags(L, s0, 0, f0x, f0w);
     jj = jn;
     J = N;
     ++tloc;
   }
+  __builtin_amdgcn_s_waitcnt(0);  // no load into LDS outlives the workgroup
 }
 
 }  // namespace

@@ -935,13 +935,21 @@ __global__ __launch_bounds__(512, 1) void transfer_bf16_tiled_kernel(const Trans
 // to global memory in the layout the staged GEMM reads.  The tile is built in
 // LDS and then written out: in the slab's [256-row tile][k-tile][256][32]
 // layout its rows are one 4 KB run per k-tile, so every wave store is 1 KB of
-// whole lines (rows past the sequence end carry zeros the GEMM never stores).  A slab is (role,
+// whole lines (rows past the sequence end carry zeros the GEMM never stores).
+// Each wave writes its own sender head as soon as its walk ends.  A slab is (role,
 // receiver layer) for the interpolating map -- x_j of Sec. 3.1 with the layer
 // weights of its two taps -- or (role, sender layer) for concatenated taps --
 // one block x_j^t of Eq. 2, shared by every receiver layer that reads that
 // sender layer.  The arithmetic is the fused kernel's build (same staging
 // record, same group walk, one bf16 rounding per feature).
 // ---------------------------------------------------------------------------
+// 16 bytes from LDS to global memory as a streaming (non-temporal) store: the
+// slab is read back only after the whole build, so it need not stay in L2.
+__device__ __forceinline__ void nt_store16(uint16_t* g, const uint16_t* l) {
+  typedef unsigned v4u __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(*reinterpret_cast<const v4u*>(l), reinterpret_cast<v4u*>(g));
+}
+
 __global__ __launch_bounds__(512) void staged_build_kernel(const TransferArgs p) {
   __shared__ __attribute__((aligned(16))) uint16_t xl[64 * kXF];  // the built tile, fused-kernel layout
   __shared__ __attribute__((aligned(16))) int ent[kRecBytes / 4];
@@ -1011,8 +1019,7 @@ __global__ __launch_bounds__(512) void staged_build_kernel(const TransferArgs p)
 #pragma unroll 4
     for (int i = 0; i < 16; ++i) {
       const int kt = 4 * wave + (i >> 2), r = 16 * (i & 3) + (lane >> 2);
-      *reinterpret_cast<uint4*>(dst + kt * (kStagedRows * 32) + r * 32 + c8) =
-          *reinterpret_cast<const uint4*>(xl + r * kXF + kt * 32 + c8);
+      nt_store16(dst + kt * (kStagedRows * 32) + r * 32 + c8, xl + r * kXF + kt * 32 + c8);
     }
   } else {
     const int r = tid >> 3;        // 8 threads per row
@@ -1029,8 +1036,7 @@ __global__ __launch_bounds__(512) void staged_build_kernel(const TransferArgs p)
     const int r2 = (tid & 255) >> 2, c8 = (tid & 3) * 8;
 #pragma unroll 4
     for (int kt = tid >> 8; kt < kHMax * kDH / 32; kt += 2)
-      *reinterpret_cast<uint4*>(dst + kt * (kStagedRows * 32) + r2 * 32 + c8) =
-          *reinterpret_cast<const uint4*>(xl + r2 * kXF + kt * 32 + c8);
+      nt_store16(dst + kt * (kStagedRows * 32) + r2 * 32 + c8, xl + r2 * kXF + kt * 32 + c8);
   }
 }
 
