@@ -38,10 +38,7 @@ PEAK_HBM_GBS = 8000.0
 PEAK_FP64_TFLOPS = 78.6     # MI355X dense fp64 matrix-core peak
 CALIB_METRIC = "calibration samples/sec for one map (moments + Recolor + fold, fp64)"
 METRIC = "receiver KV tokens/sec (all layers, K+V) at 32K; % of MFMA/HBM roofline"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "transfer_bf16_14b_32k_traffic.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_32259_amd", "csrc", "transfer.hip")
-STAGED_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "staged_gemm_14b_32k_traffic.json")
-STAGED_SOURCE = os.path.join(ROOT, "paper_2609_32259_amd", "csrc", "staged.hip")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def log(*a):
@@ -81,18 +78,24 @@ def kernel_name(cfg):
 
 
 def kernel_traffic(cfg, staged=False):
-    """HBM bytes per launch of the dominant kernel from the committed rocprofv3
-    counter summary, or None if there is none for this workload or the kernel
-    source changed since."""
-    try:
-        with open(STAGED_TRAFFIC_FILE if staged else TRAFFIC_FILE) as f:
-            rec = json.load(f)
-        src = hashlib.sha256(open(STAGED_SOURCE if staged else KERNEL_SOURCE, "rb").read()).hexdigest()
-        if rec.get("kernel_source_sha256") != src or rec.get("workload_name") != cfg.name:
-            return None
-        return rec.get("bytes_per_launch")
-    except (OSError, ValueError):
-        return None
+    """HBM bytes per launch of the dominant kernel from a committed rocprofv3
+    counter summary (profiles/*_traffic.json) of this workload and path, or
+    None if there is none or the kernel's source changed since it was taken."""
+    import glob
+    path = "staged" if staged else "fused"
+    for fn in sorted(glob.glob(os.path.join(PROFILES, "*_traffic.json"))):
+        try:
+            with open(fn) as f:
+                rec = json.load(f)
+            if rec.get("workload_name") != cfg.name or rec.get("path", "fused") != path:
+                continue
+            with open(os.path.join(ROOT, rec["kernel_source"]), "rb") as f:
+                src = hashlib.sha256(f.read()).hexdigest()
+            if rec.get("kernel_source_sha256") == src:
+                return rec.get("bytes_per_launch")
+        except (OSError, ValueError, KeyError):
+            continue
+    return None
 
 
 def cpu_model() -> str:

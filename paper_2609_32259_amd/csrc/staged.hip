@@ -16,6 +16,8 @@
 // one XCD (workgroup i runs on XCD i % 8), where they share the row tile in L2.
 #include <hip/hip_runtime.h>
 
+#include <cstddef>
+
 #include "hf_internal.h"
 
 namespace hf {
@@ -77,11 +79,23 @@ struct Lane {
 // One work item: a 256-row x 256-feature output tile of one (layer, role).
 struct Job {
   const uint16_t* wb;     // packed maps of the (layer, role), fragment order
-  const uint16_t* xt[3];  // the 256-row feature tile of each tap (1024 features, k-tile-major)
+  const uint16_t* xt0;    // the 256-row feature tile of each tap (1024 features, k-tile-major)
+  const uint16_t* xt1;
+  const uint16_t* xt2;
   const float* bias;      // the tile's 256 bias values, or nullptr
   uint16_t* rbase;        // receiver cache at (sequence, layer, role, head 2 nt, row 0)
   int nt, j0, Tr, pos0, keys;
 };
+
+// Byte i of a kernel-argument byte array, read as the aligned dword that holds
+// it: gfx950 has no scalar byte loads, and a vector load here would wait (in
+// order) for every load and store in flight.
+static_assert(offsetof(TransferArgs, taps) % 4 == 0, "taps must be dword aligned");
+FI int arg_byte(const uint8_t* base, int i) {
+  i = __builtin_amdgcn_readfirstlane(i);
+  const uint32_t w = reinterpret_cast<const uint32_t*>(base)[i >> 2];
+  return (int)((w >> (8 * (i & 3))) & 0xffu);
+}
 
 FI Job decode(const TransferArgs& p, int xcd, int jj) {
   Job J;
@@ -99,11 +113,12 @@ FI Job decode(const TransferArgs& p, int xcd, int jj) {
   J.pos0 = p.pos0_r[b];
   J.keys = c == 0;
   J.wb = static_cast<const uint16_t*>(p.Wp) + (long long)lm * (p.n_taps * 64) * 32 * 512;
-#pragma unroll
-  for (int t = 0; t < 3; ++t) {
-    const int layer = p.concat ? (int)p.taps[l][t < p.n_taps ? t : 0] : l;
-    J.xt[t] = p.xs + ((long long)c * p.n_slab_layers + layer) * p.xs_slab + (long long)rt * kSlabTile;
-  }
+  const uint16_t* xrt = p.xs + (long long)c * p.n_slab_layers * p.xs_slab + (long long)rt * kSlabTile;
+  const int t1 = p.n_taps > 1 ? 1 : 0, t2 = p.n_taps > 2 ? 2 : 0;
+  const uint8_t* tp = &p.taps[0][0];
+  J.xt0 = xrt + (long long)(p.concat ? arg_byte(tp, 3 * l) : l) * p.xs_slab;
+  J.xt1 = xrt + (long long)(p.concat ? arg_byte(tp, 3 * l + t1) : l) * p.xs_slab;
+  J.xt2 = xrt + (long long)(p.concat ? arg_byte(tp, 3 * l + t2) : l) * p.xs_slab;
   J.bias = p.bias ? p.bias + (long long)lm * 1024 + J.nt * 256 : nullptr;
   J.rbase = static_cast<uint16_t*>(p.R) + b * p.r_sb + (long long)l * p.r_sl + c * p.r_sc +
             (long long)(2 * J.nt) * p.r_sh;
@@ -125,9 +140,20 @@ FI void dma_x(const Lane& L, const uint16_t* xt, int kt, unsigned char* sb, int 
                                            (i & 1) ? L.vt1 : L.vt0, (kt & 31) * kBM * kBK * 2 + i * 1024,
                                            0, 0);
 }
+// The tap of k-tile kt.  The three pointers pass through an opaque copy before
+// the select: a select between two fields of J would otherwise become one
+// load at a computed field address, which keeps the whole work item in
+// scratch memory and stores it there once per item.
+FI const uint16_t* opaque_ptr(const uint16_t* q) {
+  asm volatile("" : "+v"(q));
+  return q;
+}
 FI const uint16_t* tap_tile(const Job& J, int kt) {
   const int t = kt >> 5;
-  return t == 0 ? J.xt[0] : t == 1 ? J.xt[1] : J.xt[2];
+  const uint16_t* a = opaque_ptr(J.xt0);
+  const uint16_t* b = opaque_ptr(J.xt1);
+  const uint16_t* c = opaque_ptr(J.xt2);
+  return t == 0 ? a : t == 1 ? b : c;
 }
 FI void dma_all(const Lane& L, const Job& J, int wbytes, int kt, unsigned char* sb) {
   dma_w(L, J.wb, wbytes, J.nt, kt, sb, 0);
@@ -381,8 +407,9 @@ __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs 
     const int jn = jj + nwl;
     const bool has_next = jn < n_jobs;
     // the last job of the workgroup loads its own first k-tiles once more into
-    // stages nothing reads again, so every k-tile issues the same loads
-    const Job N = has_next ? decode(p, xcd, jn) : J;
+    // stages nothing reads again, so every k-tile issues the same loads (the
+    // index is chosen, not the decoded item, which keeps N in registers)
+    const Job N = decode(p, xcd, has_next ? jn : jj);
     const bool rot = rope && J.keys;
     if (rot && L.wave < 4) {  // RoPE rows of this tile's 32-row block bases (rows 2 w, 2 w + 1)
       const int jb = min(J.j0 + 64 * L.wave + 32 * (L.lane >> 5), J.Tr - 1);

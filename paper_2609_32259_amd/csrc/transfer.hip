@@ -3,6 +3,8 @@
 // mean, then the folded affine map of Eq. 9 with bias and receiver RoPE in
 // the epilogue, written straight into the receiver cache layout).
 #include <hip/hip_runtime.h>
+
+#include <cstddef>
 #include <limits.h>
 
 #include <mutex>
@@ -141,14 +143,27 @@ struct Ctx {
   int Ts;
 };
 
+// Byte i of a kernel-argument byte array (lo, hi, taps), read as the aligned
+// dword that holds it with a uniform index: gfx950 has no scalar byte loads,
+// and a vector load here would wait (in order) for every load and store the
+// workgroup still has in flight, such as the previous tile's receiver rows.
+static_assert(offsetof(TransferArgs, lo) % 4 == 0 && offsetof(TransferArgs, hi) % 4 == 0 &&
+                  offsetof(TransferArgs, taps) % 4 == 0,
+              "layer-map byte arrays must be dword aligned");
+__device__ __forceinline__ int arg_byte(const uint8_t* base, int i) {
+  i = __builtin_amdgcn_readfirstlane(i);
+  const uint32_t w = reinterpret_cast<const uint32_t*>(base)[i >> 2];
+  return (int)((w >> (8 * (i & 3))) & 0xffu);
+}
+
 // Tap t of the layer map: with concatenated taps, sender layer taps[l][t]
 // with weight 1; otherwise (t = 0) the interpolation of lo and hi.
 __device__ __forceinline__ Ctx make_ctx(const TransferArgs& p, const Item& it, int t = 0) {
   Ctx x;
   const uint16_t* Sb = static_cast<const uint16_t*>(p.S) + it.b * p.s_sb + it.c * p.s_sc;
-  const int lo = p.concat ? p.taps[it.l][t] : p.lo[it.l];
+  const int lo = p.concat ? arg_byte(&p.taps[0][0], 3 * it.l + t) : arg_byte(p.lo, it.l);
   x.S_lo = Sb + (long long)lo * p.s_sl;
-  x.S_hi = Sb + (long long)(p.concat ? lo : p.hi[it.l]) * p.s_sl;
+  x.S_hi = Sb + (long long)(p.concat ? lo : arg_byte(p.hi, it.l)) * p.s_sl;
   x.cs_s = (it.c == 0 && p.unrot) ? p.cs_s + (long long)p.pos0_s[it.b] * kDH : nullptr;
   x.wlo = p.concat ? 1.0f : p.wlo[it.l];
   x.whi = p.concat ? 0.0f : p.whi[it.l];
