@@ -21,13 +21,13 @@ def torch():
     return torch
 
 
-def _compare(torch, cfg, wl, mode="overlap"):
+def _compare(torch, cfg, wl, mode="overlap", staged=None):
     from paper_2609_32259_amd.path import TransferPath
     assert wl.opts is not None
     print(f"[gpu-opts] {cfg.name} map={cfg.layer_map} post-rope keys={cfg.sender_keys_post_rope} "
-          f"B={wl.seg.batch} T_r={list(wl.seg.r_len)}", flush=True)
+          f"B={wl.seg.batch} T_r={list(wl.seg.r_len)} staged={staged}", flush=True)
     path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r, mode=mode,
-                        layer_map=cfg.layer_map, opts=wl.opts)
+                        layer_map=cfg.layer_map, opts=wl.opts, staged=staged)
     R = path.step()
     torch.cuda.synchronize()
     Case(cfg, wl, R, mode, tag="gpu-opts").check_all()
@@ -49,6 +49,18 @@ def test_opts_bf16_receiver_heads(torch, H_r):
     cfg = synth.LLAMA8B_14B_8K.with_(name=f"14b opts H_r={H_r}", H_r=H_r, T_s=300, L_r=4,
                                      paper_opts=True)
     _compare(torch, cfg, synth.make_workload(cfg, seed=32, device="cuda"))
+
+
+@pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
+def test_opts_bf16_inv_r_only(torch, staged):
+    # 1/r without the key norm: on the interpolating map the staged path serves it
+    # (the build scales the layer weights by 1/r, as the fused build does).
+    cfg = synth.LLAMA8B_14B_8K.with_(name="14b 1/r only", T_s=300, L_r=4, paper_opts=True)
+    wl = synth.make_workload(cfg, seed=34, device="cuda")
+    opts = dict(wl.opts)
+    opts["k_norm"] = None
+    _compare(torch, cfg, synth.Workload(cfg, wl.seg, wl.S, wl.A, wl.bias, wl.rope, opts),
+             staged=staged)
 
 
 @pytest.mark.parametrize("H_r", [8, 4])
