@@ -25,8 +25,9 @@ def np64(t):
 def opts64(opts):
     if opts is None:
         return None
-    return dict(inv_r=np64(opts["inv_r"]), k_norm=np64(opts["k_norm"]),
-                k_norm_eps=opts["k_norm_eps"])
+    return dict(inv_r=None if opts.get("inv_r") is None else np64(opts["inv_r"]),
+                k_norm=None if opts.get("k_norm") is None else np64(opts["k_norm"]),
+                k_norm_eps=opts.get("k_norm_eps", 1e-6))
 
 
 def seq_rope(rope, b):
