@@ -275,6 +275,26 @@ def test_bf16_equal_rope_round_trip(torch):
 
 
 @BOTH_PATHS
+def test_bf16_tile_multiple_lengths(torch, staged):
+    # Identical tokenizations in TA mode give T_r = T_s exactly: sequences of
+    # 512 and 256 rows fill whole 256-row multiply tiles, 257 and 65 rows leave
+    # one row in the last tile, and a 1-row sequence is a tile of its own.
+    cfg = synth.LLAMA8B_14B_8K.with_(name="tile-multiple lengths", L_r=3)
+    rng = np.random.default_rng(15)
+    parts = []
+    for n in (512, 256, 257, 65, 1):
+        sb, se = synth.segment_tokens(rng, n, 1, 7)
+        parts.append((sb, se, sb.copy(), se.copy()))
+    seg = synth.concat_segmentations(parts)
+    assert list(seg.r_len) == [512, 256, 257, 65, 1]
+    S = synth.make_cache(cfg, seg, seed=15, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=15, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=np.array([0, 9, 3, 100, 7], np.int32),
+                             pos0_r=np.array([4, 0, 31, 32, 5], np.int32))
+    _compare_full(torch, cfg, synth.Workload(cfg, seg, S, A, bias, rope), "ta", staged=staged)
+
+
+@BOTH_PATHS
 def test_bf16_rows_past_length_untouched_and_deterministic(torch, staged):
     cfg = synth.LLAMA8B_14B_8K.with_(T_s=260, L_r=4)
     wl = synth.make_workload(cfg, seed=8, device="cuda")
