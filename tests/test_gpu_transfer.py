@@ -295,6 +295,26 @@ def test_bf16_tile_multiple_lengths(torch, staged):
 
 
 @BOTH_PATHS
+def test_bf16_batch_of_long_ragged_sequences(torch, staged):
+    # Three sequences of several 256-row multiply tiles each, with ragged ends
+    # and per-sequence RoPE offsets: the staged path's per-sequence tile starts
+    # and slab rows well past the first tile.
+    cfg = synth.LLAMA8B_14B_8K.with_(name="three long sequences", L_r=3)
+    rng = np.random.default_rng(16)
+    parts = []
+    for n_s in (1500, 1111, 1337):
+        sb, se = synth.segment_tokens(rng, n_s, 1, 7)
+        rb, re_ = synth.segment_chars(rng, int(se[-1]), 1, 8)
+        parts.append((sb, se, rb, re_))
+    seg = synth.concat_segmentations(parts)
+    S = synth.make_cache(cfg, seg, seed=16, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=16, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=np.array([0, 40, 7], np.int32),
+                             pos0_r=np.array([3, 0, 250], np.int32))
+    _compare_full(torch, cfg, synth.Workload(cfg, seg, S, A, bias, rope), "overlap", staged=staged)
+
+
+@BOTH_PATHS
 def test_bf16_rows_past_length_untouched_and_deterministic(torch, staged):
     cfg = synth.LLAMA8B_14B_8K.with_(T_s=260, L_r=4)
     wl = synth.make_workload(cfg, seed=8, device="cuda")
