@@ -265,14 +265,17 @@ size_t hf_transfer_workspace_bytes(int32_t B, const int32_t* s_len, const int32_
  * the staged path does not apply: it serves bf16 with 8 sender and 8 receiver
  * heads of d_h = 128.
  * The transfer calls take the staged path when their workspace holds at least
- * this many bytes, the shape is served, opts->k_norm is NULL, (for
- * concatenated taps, whose slabs several receiver layers share) opts->inv_r is
- * NULL, and every sequence's receiver rows span less than 2 GiB of its cache
- * (the multiply addresses them with 32-bit byte offsets); otherwise the fused
- * path.  Both compute the same values up to the order of the fp32
- * accumulation: the staged path builds x_j exactly as the fused path does (one
- * bf16 rounding), stores it, and multiplies it in a separate kernel.
- * hf_transfer_kv_noalloc always takes the fused path.
+ * this many bytes, the shape is served, and every sequence's receiver rows
+ * span less than 2 GiB of its cache (the multiply addresses them with 32-bit
+ * byte offsets); otherwise the fused path.  Both compute the same values up to
+ * rounding: the staged path builds x_j as the fused path does (one bf16
+ * rounding), stores it, and multiplies it in a separate kernel whose epilogue
+ * applies the bias, the key norm and the receiver RoPE.  One difference in
+ * where rounding happens: with concatenated taps the slabs are shared by
+ * receiver layers with different r, so the staged path rounds x_j without
+ * 1/r and scales the product A x_j by 1/r in fp32, where the fused path
+ * rounds x_j / r (equal in exact arithmetic).  hf_transfer_kv_noalloc always
+ * takes the fused path.
  */
 size_t hf_transfer_staged_workspace_bytes(int32_t B, const int32_t* s_len, const int32_t* r_len,
                                           const hf_kv_desc* sender, const hf_kv_desc* receiver,

@@ -540,8 +540,7 @@ int32_t transfer_impl(int32_t B, const int32_t* s_len, const int32_t* r_len,
   // The staged path, where it applies and the workspace holds its slabs.
   bool staged = false;
   size_t st_need = 0;
-  if (!noalloc && hf::staged_supported(dtype, sender->H, receiver->H, d_h) && ws_need > 0 &&
-      !(opts && opts->k_norm) && !(ls.concat && opts && opts->inv_r)) {
+  if (!noalloc && hf::staged_supported(dtype, sender->H, receiver->H, d_h) && ws_need > 0) {
     st_need = ws_need + staged_extra_bytes(B, r_len, ls.concat ? L_s : L_r);
     staged = workspace_bytes >= st_need;
     for (int b = 0; staged && b < B; ++b)  // receiver rows are addressed with 32-bit byte offsets

@@ -84,7 +84,7 @@ struct Job {
   const uint16_t* xt2;
   const float* bias;      // the tile's 256 bias values, or nullptr
   uint16_t* rbase;        // receiver cache at (sequence, layer, role, head 2 nt, row 0)
-  int nt, j0, Tr, pos0, keys;
+  int nt, j0, Tr, pos0, keys, l;
 };
 
 // Byte i of a kernel-argument byte array, read as the aligned dword that holds
@@ -120,6 +120,7 @@ FI Job decode(const TransferArgs& p, int xcd, int jj) {
   J.xt1 = xrt + (long long)(p.concat ? arg_byte(tp, 3 * l + t1) : l) * p.xs_slab;
   J.xt2 = xrt + (long long)(p.concat ? arg_byte(tp, 3 * l + t2) : l) * p.xs_slab;
   J.bias = p.bias ? p.bias + (long long)lm * 1024 + J.nt * 256 : nullptr;
+  J.l = l;
   J.rbase = static_cast<uint16_t*>(p.R) + b * p.r_sb + (long long)l * p.r_sl + c * p.r_sc +
             (long long)(2 * J.nt) * p.r_sh;
   return J;
@@ -261,13 +262,32 @@ FI void rope_cs(const Lane& L, const float* st0row, const float* st1, int qq, in
 // 128-byte row halves.  Staging row rr keeps its 16-byte chunk c at slot
 // c ^ ((rr >> 1) & 7): the 32 rows of one 8-byte write then cover 16 distinct
 // 16-byte bank groups, the most a 128-byte row stride allows.
-template <bool ROT, int m>
+template <bool ROT, bool KN, int m>
 FI void epi_block(const Lane& L, const f32x16 (&acc)[kMB][4], int j0, int Tr, long long r_st,
-                  const float* bsh, uint16_t* stg, __amdgpu_buffer_rsrc_t rR, const float* st0,
-                  const float* st1) {
+                  const float* bsh, float scale, const float* knh, float eps, uint16_t* stg,
+                  __amdgpu_buffer_rsrc_t rR, const float* st0, const float* st1) {
   const int rr = L.lane & 31;
   float keep[2][4][4];
   uint2 v0[2][4];
+  float inv = 1.0f;
+  if (KN) {  // receiver key RMSNorm over the head's 128 features (lanes l and l ^ 32)
+    float ss = 0.0f;
+#pragma unroll
+    for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(bsh + 32 * qq + 8 * g);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(bsh + 64 + 32 * qq + 8 * g);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float y0 = fmaf(acc[m][qq][4 * g + u], scale, b0[u]);
+          const float y1 = fmaf(acc[m][qq + 2][4 * g + u], scale, b1[u]);
+          ss = fmaf(y0, y0, fmaf(y1, y1, ss));
+        }
+      }
+    ss += __shfl_xor(ss, 32);
+    inv = 1.0f / sqrtf(ss * (1.0f / 128) + eps);
+  }
 #pragma unroll
   for (int qq = 0; qq < 2; ++qq)
 #pragma unroll
@@ -277,8 +297,17 @@ FI void epi_block(const Lane& L, const f32x16 (&acc)[kMB][4], int j0, int Tr, lo
       float p0[4], p1[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        p0[u] = acc[m][qq][4 * g + u] + b0[u];
-        p1[u] = acc[m][qq + 2][4 * g + u] + b1[u];
+        p0[u] = fmaf(acc[m][qq][4 * g + u], scale, b0[u]);
+        p1[u] = fmaf(acc[m][qq + 2][4 * g + u], scale, b1[u]);
+      }
+      if (KN) {
+        const f32x4 w0 = *reinterpret_cast<const f32x4*>(knh + 32 * qq + 8 * g);
+        const f32x4 w1 = *reinterpret_cast<const f32x4*>(knh + 64 + 32 * qq + 8 * g);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          p0[u] *= inv * w0[u];
+          p1[u] *= inv * w1[u];
+        }
       }
       if (ROT) {
         f32x4 cv, sv;
@@ -329,26 +358,31 @@ FI void epi_block(const Lane& L, const f32x16 (&acc)[kMB][4], int j0, int Tr, lo
   }
 }
 
-template <bool ROT>
+template <bool ROT, bool KN>
 FI void epilogue(const Lane& L0, const f32x16 (&acc)[kMB][4], int j0, int Tr, long long r_st,
-                 const float* bias_base, uint16_t* stg, __amdgpu_buffer_rsrc_t rR, const float* st0,
-                 const float* st1) {
+                 const float* bias_base, float scale, const float* kn_base, float eps,
+                 uint16_t* stg, __amdgpu_buffer_rsrc_t rR, const float* st0, const float* st1) {
   // lane-derived addresses are formed here, inside the work-item loop, so that
   // they are not hoisted out of it and held across the k-loop
   Lane L = L0;
   L.lane = opaque(L0.lane);
   L.hi4 = 4 * (L.lane >> 5);
   const float* bsh = bias_base + 128 * L.wc + L.hi4;
-  epi_block<ROT, 0>(L, acc, j0, Tr, r_st, bsh, stg, rR, st0, st1);
-  epi_block<ROT, 1>(L, acc, j0, Tr, r_st, bsh, stg, rR, st0, st1);
+  const float* knh = kn_base + L.hi4;
+  epi_block<ROT, KN, 0>(L, acc, j0, Tr, r_st, bsh, scale, knh, eps, stg, rR, st0, st1);
+  epi_block<ROT, KN, 1>(L, acc, j0, Tr, r_st, bsh, scale, knh, eps, stg, rR, st0, st1);
 }
 
+// KN: the receiver key norm is on (keys of calls that pass its weights); a
+// separate instantiation keeps its registers out of the common kernel.
+template <bool KN>
 __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs p) {
   __shared__ __attribute__((aligned(1024))) unsigned char s0[32768];
   __shared__ __attribute__((aligned(1024))) unsigned char s1[32768];
   __shared__ __attribute__((aligned(1024))) unsigned char s2[32768];
   __shared__ __attribute__((aligned(1024))) unsigned char s3[32768];
   __shared__ __attribute__((aligned(1024))) float sbias[2 * 256];  // double-buffered tile bias
+  __shared__ __attribute__((aligned(1024))) float skn[2 * 128];    // double-buffered key-norm weights
   __shared__ __attribute__((aligned(1024))) float st1[32 * 128];   // RoPE rows 0..31, swizzled
   __shared__ __attribute__((aligned(1024))) float st0[8 * 128];    // RoPE rows of the 8 block bases
 
@@ -383,9 +417,12 @@ __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs 
   dma_all(L, J, wbytes, 0, s0);
   dma_all(L, J, wbytes, 1, s1);
   dma_all(L, J, wbytes, 2, s2);
-  auto dma_bias = [&](const Job& T, int half) {
+  auto dma_bias = [&](const Job& T, int half) {  // and the key-norm weights
     if (L.wave == 0 && T.bias)
       __builtin_amdgcn_global_load_lds(T.bias + L.lane * 4, (lds_void_t*)(sbias + half * 256), 16, 0, 0);
+    if (KN && L.wave == 1 && T.keys && L.lane < 32)
+      __builtin_amdgcn_global_load_lds(p.k_norm + T.l * 128 + L.lane * 4, (lds_void_t*)(skn + half * 128),
+                                       16, 0, 0);
   };
   dma_bias(J, 0);
   if (!p.bias) sbias[threadIdx.x] = 0.0f;
@@ -443,8 +480,19 @@ __global__ __launch_bounds__(512, 1) void staged_gemm_kernel(const TransferArgs 
           mk_rsrc(J.rbase + (long long)L.wc * p.r_sh, (int)((long long)J.Tr * p.r_st * 2));
       uint16_t* stg = reinterpret_cast<uint16_t*>(s3) + L.wave * 32 * 64;  // stage 3 is free here
       const float* bias_base = sbias + (tloc & 1) * 256;
-      if (rot) epilogue<true>(L, acc, J.j0, J.Tr, p.r_st, bias_base, stg, rR, st0, st1);
-      else epilogue<false>(L, acc, J.j0, J.Tr, p.r_st, bias_base, stg, rR, st0, st1);
+      const float* kn_base = skn + (tloc & 1) * 128;
+      const float eps = p.k_norm_eps;
+      // With concatenated taps the slabs are shared by receiver layers with
+      // different r, so 1/r scales the product A x_j (equal to A (x_j / r));
+      // the interpolating build already scaled x_j.
+      const float scale = (p.inv_r && p.concat) ? p.inv_r[J.l * 2 + (J.keys ? 0 : 1)] : 1.0f;
+      if (KN && J.keys) {
+        if (rot) epilogue<true, true>(L, acc, J.j0, J.Tr, p.r_st, bias_base, scale, kn_base, eps, stg, rR, st0, st1);
+        else epilogue<false, true>(L, acc, J.j0, J.Tr, p.r_st, bias_base, scale, kn_base, eps, stg, rR, st0, st1);
+      } else {
+        if (rot) epilogue<true, false>(L, acc, J.j0, J.Tr, p.r_st, bias_base, scale, kn_base, eps, stg, rR, st0, st1);
+        else epilogue<false, false>(L, acc, J.j0, J.Tr, p.r_st, bias_base, scale, kn_base, eps, stg, rR, st0, st1);
+      }
     }
     if (!has_next) break;
     // The next job's bias goes into the other half of sbias only now: a load
@@ -470,7 +518,8 @@ hipError_t launch_staged_gemm(const TransferArgs& a, hipStream_t s) {
   if (e == hipSuccess) e = hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
   const int grid = 8 * std::max(1, n_cu / 8);  // whole XCD rounds: workgroup i runs on XCD i % 8
-  hipLaunchKernelGGL(staged_gemm_kernel, dim3((unsigned)grid), dim3(512), 0, s, a);
+  if (a.k_norm) hipLaunchKernelGGL(staged_gemm_kernel<true>, dim3((unsigned)grid), dim3(512), 0, s, a);
+  else hipLaunchKernelGGL(staged_gemm_kernel<false>, dim3((unsigned)grid), dim3(512), 0, s, a);
   return hipGetLastError();
 }
 

@@ -67,16 +67,10 @@ class TransferPath:
         # staged=None picks the faster path as measured at 32K on one MI355X:
         # staged for concatenated taps, fused for the interpolating map.
         wsb = hf.hf_transfer_workspace_bytes(self.s_len, self.r_len, S, R, self.rope)
-        # The library serves the key norm, and 1/r with concatenated taps, on the
-        # fused path only.
-        o = opts or {}
-        opts_ok = o.get("k_norm") is None and not (layer_map == "neighbor3"
-                                                   and o.get("inv_r") is not None)
         if staged is None:
-            staged = layer_map == "neighbor3" and opts_ok and hf.hf_transfer_staged_workspace_bytes(
+            staged = layer_map == "neighbor3" and hf.hf_transfer_staged_workspace_bytes(
                 self.s_len, self.r_len, S, R, self.rope, 3) > 0
-        if staged and not opts_ok:
-            raise ValueError("the staged path does not serve these transfer options")
+        self.staged = bool(staged)  # the path the library takes for this batch
         if staged:
             n_taps = 3 if layer_map == "neighbor3" else 0
             st = hf.hf_transfer_staged_workspace_bytes(self.s_len, self.r_len, S, R, self.rope,

@@ -63,10 +63,15 @@ def windows(T_r, tile, rng, n_mid=2, width=256):
 class Case:
     """One GPU result to check: cfg, workload, the receiver cache R the path
     wrote, the alignment mode and the layer map ("interp2", "neighbor3" or an
-    explicit [L_r][n] tap table)."""
+    explicit [L_r][n] tap table).  scale_product: the path applied 1/r to the
+    product A x_j instead of to x_j before its bf16 rounding (the staged path
+    with concatenated taps); the kernel-arithmetic gate then rounds x_j unscaled
+    and maps it with A / r."""
 
-    def __init__(self, cfg, wl, R, mode="overlap", layer_map=None, tag="gpu"):
+    def __init__(self, cfg, wl, R, mode="overlap", layer_map=None, tag="gpu",
+                 scale_product=False):
         self.cfg, self.wl, self.R, self.mode, self.tag = cfg, wl, R, mode, tag
+        self.scale_product = scale_product
         lmap = cfg.layer_map if layer_map is None else layer_map
         if isinstance(lmap, str) and lmap == "interp2":
             self.lt, self.taps = lm.interp2(cfg.L_s, cfg.L_r), None
@@ -122,7 +127,13 @@ class Case:
                 where = f"{cfg.name} b={b} l={l} c={c} rows=[{r0},{r1})"
                 gate = None
                 if cfg.dtype == "bf16":
-                    gate = kernel_gate(xs, A, bias, c, cfg.d_h, l, rope, self.opts, rows)
+                    inv_r = None if self.opts is None else self.opts.get("inv_r")
+                    if self.scale_product and inv_r is not None:
+                        o = dict(self.opts, inv_r=None)
+                        gate = kernel_gate(np.asarray(x, np.float64), A * float(inv_r[l, c]), bias, c,
+                                           cfg.d_h, l, rope, o, rows)
+                    else:
+                        gate = kernel_gate(xs, A, bias, c, cfg.d_h, l, rope, self.opts, rows)
                 s = check_layer(got, ref, where, dtype=cfg.dtype,
                                 max_abs="report" if self.qlimited(c) else "ulp", gate=gate)
                 worst.add(s)

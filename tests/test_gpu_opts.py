@@ -30,7 +30,8 @@ def _compare(torch, cfg, wl, mode="overlap", staged=None):
                         layer_map=cfg.layer_map, opts=wl.opts, staged=staged)
     R = path.step()
     torch.cuda.synchronize()
-    Case(cfg, wl, R, mode, tag="gpu-opts").check_all()
+    Case(cfg, wl, R, mode, tag="gpu-opts",
+         scale_product=path.staged and cfg.layer_map == "neighbor3").check_all()
 
 
 def test_opts_fp32(torch):
@@ -63,24 +64,36 @@ def test_opts_bf16_inv_r_only(torch, staged):
              staged=staged)
 
 
-@pytest.mark.parametrize("H_r", [8, 4])
-def test_opts_bf16_paper_construction(torch, H_r):
+@pytest.mark.parametrize("H_r,staged", [(8, False), (8, True), (4, False)])
+def test_opts_bf16_paper_construction(torch, H_r, staged):
+    # With 8 receiver heads both paths: on the staged path the key norm runs in
+    # the multiply's epilogue and 1/r scales the product (the slabs of
+    # concatenated taps are shared by receiver layers with different r).
     cfg = synth.LLAMA8B_14B_32K_PAPER.with_(name=f"paper small H_r={H_r}", H_r=H_r, T_s=350,
                                             L_r=5)
-    _compare(torch, cfg, synth.make_workload(cfg, seed=33, device="cuda"))
+    _compare(torch, cfg, synth.make_workload(cfg, seed=33, device="cuda"), staged=staged)
 
 
-def test_full_14b_shape_32k_paper_construction(torch):
+@pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
+def test_opts_bf16_key_norm_interpolating(torch, staged):
+    # The key norm and 1/r on the interpolating map (the staged build scales the
+    # features by 1/r; the multiply's epilogue normalizes the keys).
+    cfg = synth.LLAMA8B_14B_8K.with_(name="14b key norm", T_s=300, L_r=4, paper_opts=True)
+    _compare(torch, cfg, synth.make_workload(cfg, seed=35, device="cuda"), staged=staged)
+
+
+@pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
+def test_full_14b_shape_32k_paper_construction(torch, staged):
     """The benchmark's paper-construction workload: every layer and role, on
-    windows of rows."""
+    windows of rows, on both paths."""
     from paper_2609_32259_amd.path import TransferPath
     cfg = synth.LLAMA8B_14B_32K_PAPER
     wl = synth.make_workload(cfg, seed=0, device="cuda")
-    print(f"[gpu-opts] full-size {cfg.name} T_r={list(wl.seg.r_len)}", flush=True)
+    print(f"[gpu-opts] full-size {cfg.name} T_r={list(wl.seg.r_len)} staged={staged}", flush=True)
     path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r,
-                        layer_map=cfg.layer_map, opts=wl.opts)
+                        layer_map=cfg.layer_map, opts=wl.opts, staged=staged)
     R = path.step()
     torch.cuda.synchronize()
     rng = np.random.default_rng(97)
-    Case(cfg, wl, R, tag="gpu-opts-32k").check_all(
+    Case(cfg, wl, R, tag="gpu-opts-32k", scale_product=path.staged).check_all(
         windows_of=lambda b, T_r: windows(T_r, 64, rng, n_mid=2, width=384))

@@ -62,10 +62,14 @@ def _f32_rotate(y, pos, theta):
     return np.concatenate([y1 * c - y2 * s, y2 * c + y1 * s], axis=-1)
 
 
-def _emulate(xs, A_lc, b_lc, role, layer, rope, opts, rows, rope_shift=0):
-    """The path's arithmetic on scaled features xs (fp64 [n, K])."""
+def _emulate(xs, A_lc, b_lc, role, layer, rope, opts, rows, rope_shift=0, product_scale=None):
+    """The path's arithmetic on scaled features xs (fp64 [n, K]); with
+    product_scale, the fp32 product is multiplied by it before the bias (the
+    staged path's 1/r with concatenated taps)."""
     xb = bf16_round(xs).astype(np.float32)
     y = xb @ A_lc.astype(np.float32).T
+    if product_scale is not None:
+        y = y * np.float32(product_scale)
     if b_lc is not None:
         y = y + b_lc.astype(np.float32)[None, :]
     n = xs.shape[0]
@@ -157,6 +161,36 @@ def test_planted_mistake_fails_the_gate(wl, plant):
     assert np.any(np.abs(got - ref_q) > bound), plant
     with pytest.raises(AssertionError):
         check_layer(got, ref, plant, max_abs="report", gate=gate)
+
+
+def _paper_opts():
+    opts = synth.make_opts(CFG.with_(paper_opts=True), seed=21, device="cpu")
+    return dict(inv_r=opts["inv_r"].numpy().astype(np.float64),
+                k_norm=opts["k_norm"].numpy().astype(np.float64), k_norm_eps=opts["k_norm_eps"])
+
+
+def test_scaled_product_passes_its_gate_and_planted_scales_fail(wl):
+    # The staged path with concatenated taps rounds x_j without 1/r and scales
+    # the product A x_j by 1/r: the gate then rounds x_j unscaled and maps it
+    # with A / r (equal to the oracle's A (x_j / r) in exact arithmetic).
+    opts = _paper_opts()
+    layer, role = 3, 0
+    S, csr, lt, rope, A, b = _inputs(wl)
+    rows = np.arange(csr[0].size - 1)
+    x = tr.features(S, lt, csr, rope, layer, role)
+    inv = float(opts["inv_r"][layer, role])
+    ref = tr.map_features(tr.scaled_features(x, layer, role, opts), A[layer, role], b[layer, role],
+                          role, CFG.d_h, layer, rope, opts)
+    o = dict(opts, inv_r=None)
+    gate = kernel_gate(x, A[layer, role] * inv, b[layer, role], role, CFG.d_h, layer, rope, o)
+    got = _emulate(x, A[layer, role], b[layer, role], role, layer, rope, o, rows, product_scale=inv)
+    s = check_layer(got, ref, "scaled product", max_abs="report", gate=gate)
+    assert s["gate"] <= 1.0
+    ref_q, bound = gate
+    for bad in (1.0, inv * inv):  # 1/r left out, 1/r applied twice
+        got = _emulate(x, A[layer, role], b[layer, role], role, layer, rope, o, rows,
+                       product_scale=bad)
+        assert np.any(np.abs(got - ref_q) > bound), bad
 
 
 def test_planted_mistakes_fail_with_key_norm(wl):
