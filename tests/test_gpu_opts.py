@@ -64,6 +64,18 @@ def test_opts_bf16_inv_r_only(torch, staged):
              staged=staged)
 
 
+@pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
+def test_opts_bf16_taps_inv_r_only(torch, staged):
+    # Concatenated taps with 1/r and no key norm: on the staged path the common
+    # multiply kernel scales the product by 1/r.
+    cfg = synth.LLAMA8B_14B_32K_PAPER.with_(name="paper taps 1/r only", T_s=330, L_r=5)
+    wl = synth.make_workload(cfg, seed=36, device="cuda")
+    opts = dict(wl.opts)
+    opts["k_norm"] = None
+    _compare(torch, cfg, synth.Workload(cfg, wl.seg, wl.S, wl.A, wl.bias, wl.rope, opts),
+             staged=staged)
+
+
 @pytest.mark.parametrize("H_r,staged", [(8, False), (8, True), (4, False)])
 def test_opts_bf16_paper_construction(torch, H_r, staged):
     # With 8 receiver heads both paths: on the staged path the key norm runs in
