@@ -207,6 +207,32 @@ def test_transfer_workspace_records(L):
     assert call(C.c_void_p(0x100000 + 16), 1 << 20) == -2   # not 256-byte aligned
 
 
+def test_transfer_staged_workspace_bytes(L):
+    # The staged path's size: the fused path's workspace, a 16 KB table, and one
+    # slab per (role, receiver layer) -- interpolating map -- or per (role, sender
+    # layer) -- concatenated taps -- of 2 bytes x 1024 features x 256 rows per
+    # 256-row tile of each sequence.
+    s_len = np.array([64, 64, 700], np.int32)
+    r_len = np.array([60, 0, 513], np.int32)     # 1 + 0 + 3 row tiles of 256
+    sd, rd = _desc(L_=4, T=1024), _desc(L_=6, T=1024)
+
+    def st(n_taps, sd=sd, rd=rd, B=3):
+        return L.hf_transfer_staged_workspace_bytes(B, _p(s_len), _p(r_len), C.byref(sd),
+                                                    C.byref(rd), None, n_taps)
+
+    base = L.hf_transfer_workspace_bytes(3, _p(s_len), _p(r_len), C.byref(sd), C.byref(rd), None)
+    slab = 4 * 256 * 1024 * 2
+    assert st(0) == base + 16384 + 2 * 6 * slab          # receiver layers
+    for n_taps in (1, 2, 3):
+        assert st(n_taps) == base + 16384 + 2 * 4 * slab  # sender layers
+    # shapes and arguments the staged path does not serve
+    assert st(4) == 0 and st(-1) == 0 and st(0, B=0) == 0
+    assert st(0, rd=_desc(L_=6, H=4, T=1024)) == 0            # 4 receiver heads
+    assert st(0, sd=_desc(L_=4, H=16, T=1024)) == 0           # 16 sender heads
+    assert st(0, sd=_desc(L_=4, dtype=0, T=1024), rd=_desc(L_=6, dtype=0, T=1024)) == 0  # fp32
+    assert st(0, sd=_desc(L_=4, d=64, T=1024), rd=_desc(L_=6, d=64, T=1024)) == 0     # d_h 64
+
+
 def test_pack_host_validation(L):
     fake = C.c_void_p(0x1000)
     assert L.hf_pack_maps(2, 100, 1024, 1, fake, C.c_void_p(0x100000), None) == -2   # d_r % 32
