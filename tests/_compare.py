@@ -7,7 +7,9 @@ features_taps on the sliced sender cache, with the sender RoPE positions
 shifted to match), then mapped (oracle.transfer.map_features), and every
 element of the GPU result in the window is checked by _parity.check_layer.
 Windows keep full-size checks affordable: the oracle's cost grows with the
-window, not with the sequence.
+windows, not with the sequence.  The windows of a sequence are mapped, gated
+and compared together, so a per-layer figure such as rel-Fro covers all of
+them.
 """
 
 import numpy as np
@@ -61,16 +63,18 @@ def windows(T_r, tile, rng, n_mid=2, width=256):
 
 
 class Case:
-    """One GPU result to check: cfg, workload, the receiver cache R the path
-    wrote, the alignment mode and the layer map ("interp2", "neighbor3" or an
-    explicit [L_r][n] tap table).  scale_product: the path applied 1/r to the
-    product A x_j instead of to x_j before its bf16 rounding (the staged path
-    with concatenated taps); the kernel-arithmetic gate then rounds x_j unscaled
-    and maps it with A / r."""
+    """GPU results to check: cfg, workload, the receiver cache R a path wrote
+    (or a dict {label: R} of several paths' caches for the same inputs, each
+    checked against one oracle computation), the alignment mode and the layer
+    map ("interp2", "neighbor3" or an explicit [L_r][n] tap table).
+    scale_product: the path applied 1/r to the product A x_j instead of to x_j
+    before its bf16 rounding (the staged path with concatenated taps); the
+    kernel-arithmetic gate then rounds x_j unscaled and maps it with A / r."""
 
     def __init__(self, cfg, wl, R, mode="overlap", layer_map=None, tag="gpu",
                  scale_product=False):
-        self.cfg, self.wl, self.R, self.mode, self.tag = cfg, wl, R, mode, tag
+        self.cfg, self.wl, self.mode, self.tag = cfg, wl, mode, tag
+        self.results = dict(R) if isinstance(R, dict) else {"": R}
         self.scale_product = scale_product
         lmap = cfg.layer_map if layer_map is None else layer_map
         if isinstance(lmap, str) and lmap == "interp2":
@@ -93,17 +97,27 @@ class Case:
         return c == 0 and cfg.dtype == "bf16" and (bool(cfg.k_scale_sigma) or
                                                    self.opts is not None)
 
-    def check(self, b, layers, r0=0, r1=None, roles=(0, 1), worst=None, verbose=False):
+    def check(self, b, layers, spans=None, roles=(0, 1), worst=None, verbose=False):
+        """Sequence b, the given receiver layers and roles, on the row windows
+        spans [(r0, r1), ...] (the whole sequence by default).  Each window's
+        features are formed from the sender tokens it reads; the windows' rows
+        are then mapped, gated and compared together, one oracle map and one
+        gate per (layer, role), with rel-Fro over all of them."""
         cfg, wl = self.cfg, self.wl
         T_r = int(wl.seg.r_len[b])
-        r1 = T_r if r1 is None else r1
+        spans = [(0, T_r)] if spans is None else spans
+        spans = [(r0, min(r1, T_r)) for r0, r1 in spans if min(r1, T_r) > r0]
         worst = Worst() if worst is None else worst
-        if T_r == 0 or r1 <= r0:
+        if not spans:
             return worst
-        csr_w, c0, c1 = csr_window(self.csr(b), r0, r1)
         rope = seq_rope(wl.rope, b)
-        rope_w = None if rope is None else dict(rope, pos0_s=rope["pos0_s"] + c0)
-        rows = np.arange(r0, r1)
+        win = []  # (r0, r1, csr_w, c0, c1, rope_w) per window
+        for r0, r1 in spans:
+            csr_w, c0, c1 = csr_window(self.csr(b), r0, r1)
+            win.append((r0, r1, csr_w, c0, c1,
+                        None if rope is None else dict(rope, pos0_s=rope["pos0_s"] + c0)))
+        rows = np.concatenate([np.arange(r0, r1) for r0, r1 in spans])
+        span_txt = ",".join(f"[{r0},{r1})" for r0, r1 in spans)
         A_all, b_all = wl.A, wl.bias
         for l in layers:
             if self.taps is None:
@@ -113,18 +127,20 @@ class Case:
             else:
                 need = sorted(set(int(t) for t in self.taps[l]))
                 sub = np.array([[need.index(int(t)) for t in self.taps[l]]])
-            S = np64(wl.S[b, need][:, :, :, c0:c1, :])
+            # the windows' sender columns only, both roles
+            S_w = [np64(wl.S[b][:, :, :, c0:c1, :][need]) for _, _, _, c0, c1, _ in win]
             for c in roles:
-                if self.taps is None:
-                    x = tr.features(S, sub, csr_w, rope_w, 0, c)
-                else:
-                    x = tr.features_taps(S, sub, csr_w, rope_w, 0, c)
+                parts = []
+                for S, (_, _, csr_w, _, _, rope_w) in zip(S_w, win):
+                    if self.taps is None:
+                        parts.append(tr.features(S, sub, csr_w, rope_w, 0, c))
+                    else:
+                        parts.append(tr.features_taps(S, sub, csr_w, rope_w, 0, c))
+                x = np.concatenate(parts, axis=0)
                 xs = tr.scaled_features(x, l, c, self.opts)
                 A = np64(A_all[l, c])
                 bias = None if b_all is None else np64(b_all[l, c])
                 ref = tr.map_features(xs, A, bias, c, cfg.d_h, l, rope, self.opts, rows)
-                got = np64(self.R[b, l, c, :, r0:r1, :])
-                where = f"{cfg.name} b={b} l={l} c={c} rows=[{r0},{r1})"
                 gate = None
                 if cfg.dtype == "bf16":
                     inv_r = None if self.opts is None else self.opts.get("inv_r")
@@ -134,13 +150,16 @@ class Case:
                                            cfg.d_h, l, rope, o, rows)
                     else:
                         gate = kernel_gate(xs, A, bias, c, cfg.d_h, l, rope, self.opts, rows)
-                s = check_layer(got, ref, where, dtype=cfg.dtype,
-                                max_abs="report" if self.qlimited(c) else "ulp", gate=gate)
-                worst.add(s)
-                if verbose:
-                    print(f"[{self.tag}] {where}: rel-Fro {s['rel']:.3e} max|err| {s['max']:.3e} "
-                          f"#>2e-2 {s['n_over']} #>2e-2+ulp {s['n_over_ulp']} "
-                          f"gate {s['gate']:.2f}", flush=True)
+                for label, R in self.results.items():
+                    got = np.concatenate([np64(R[b, l, c, :, r0:r1, :]) for r0, r1 in spans], axis=1)
+                    where = f"{cfg.name}{' ' + label if label else ''} b={b} l={l} c={c} rows={span_txt}"
+                    s = check_layer(got, ref, where, dtype=cfg.dtype,
+                                    max_abs="report" if self.qlimited(c) else "ulp", gate=gate)
+                    worst.add(s)
+                    if verbose:
+                        print(f"[{self.tag}] {where}: rel-Fro {s['rel']:.3e} max|err| {s['max']:.3e} "
+                              f"#>2e-2 {s['n_over']} #>2e-2+ulp {s['n_over_ulp']} "
+                              f"gate {s['gate']:.2f}", flush=True)
         return worst
 
     def check_all(self, layers=None, windows_of=None, verbose=False):
@@ -150,8 +169,7 @@ class Case:
         layers = range(self.cfg.L_r) if layers is None else layers
         for b in range(self.wl.seg.batch):
             T_r = int(self.wl.seg.r_len[b])
-            spans = [(0, T_r)] if windows_of is None else windows_of(b, T_r)
-            for r0, r1 in spans:
-                self.check(b, layers, r0, r1, worst=worst, verbose=verbose)
+            spans = None if windows_of is None else windows_of(b, T_r)
+            self.check(b, layers, spans, worst=worst, verbose=verbose)
         print(f"[{self.tag}] {self.cfg.name}: {worst}", flush=True)
         return worst

@@ -97,8 +97,10 @@ def kernel_gate(xs, A_lc, b_lc, role, d_h, layer=0, rope=None, opts=None, rows=N
     r, c = np.nonzero(near_midpoint(xs))
     flip = sp.csr_matrix((bf16_ulp(xs[r, c]), (r, c)), shape=(n, K)) @ np.abs(A).T
     e = _t(flip)
-    e += K * 2.0 ** -24 * torch.outer(_t(np.linalg.norm(xq, axis=1)), _t(np.linalg.norm(A, axis=1)))
-    y = _t(xq @ A.T)
+    xq_t, A_t = _t(xq), _t(A)
+    e += K * 2.0 ** -24 * torch.outer(torch.linalg.vector_norm(xq_t, dim=1),
+                                      torch.linalg.vector_norm(A_t, dim=1))
+    y = xq_t @ A_t.T
     if b_lc is not None:
         bb = _t(b_lc)[None, :]
         y += bb

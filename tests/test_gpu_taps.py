@@ -153,14 +153,15 @@ def test_taps_bf16_identity_first_block_is_bit_exact(torch, staged):
                                wl.S[0, int(taps[l, 0]), :, :, :150, :].view(torch.int16))
 
 
-@BOTH_PATHS
-def test_full_14b_shape_32k_neighbor3(torch, staged):
-    """The benchmark's neighbourhood-map workload (the staged path is the
-    benchmark's): every layer and role, on windows of rows."""
+def test_full_14b_shape_32k_neighbor3(torch):
+    """The benchmark's neighbourhood-map workload on both paths (the staged
+    path is the benchmark's): every layer and role, on windows of rows, each
+    window's oracle result checking both."""
     cfg = synth.LLAMA8B_14B_32K_N3
     wl = synth.make_workload(cfg, seed=0, device="cuda")
-    print(f"[gpu-taps] full-size {cfg.name} T_r={list(wl.seg.r_len)} staged={staged}", flush=True)
-    path = _run(torch, cfg, wl, "overlap", None, staged=staged)
+    print(f"[gpu-taps] full-size {cfg.name} T_r={list(wl.seg.r_len)}, both paths", flush=True)
+    R = {"fused": _run(torch, cfg, wl, "overlap", None, staged=False).R,
+         "staged": _run(torch, cfg, wl, "overlap", None, staged=True).R}
     rng = np.random.default_rng(98)
-    Case(cfg, wl, path.R, tag="gpu-taps-32k").check_all(
+    Case(cfg, wl, R, tag="gpu-taps-32k").check_all(
         windows_of=lambda b, T_r: windows(T_r, 64, rng, n_mid=2, width=384))
