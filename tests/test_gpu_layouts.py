@@ -31,16 +31,16 @@ def torch():
     return torch
 
 
-def _token_major(torch, shape):
+def _token_major(torch, shape, dtype):
     """A zeroed head-major view [B, L, 2, H, T, d] of token-major storage."""
     B, L, two, H, T, d = shape
-    st = torch.zeros((B, L, two, T, H, d), dtype=torch.bfloat16, device="cuda")
+    st = torch.zeros((B, L, two, T, H, d), dtype=dtype, device="cuda")
     return st.permute(0, 1, 2, 4, 3, 5), st
 
 
-def _padded(torch, shape, pad_fill=0.0):
+def _padded(torch, shape, dtype, pad_fill=0.0):
     """A zeroed view of rows padded by PAD elements, the padding set to pad_fill."""
-    st = torch.zeros(tuple(shape[:-1]) + (shape[-1] + PAD,), dtype=torch.bfloat16, device="cuda")
+    st = torch.zeros(tuple(shape[:-1]) + (shape[-1] + PAD,), dtype=dtype, device="cuda")
     st[..., shape[-1]:] = pad_fill
     return st[..., : shape[-1]], st
 
@@ -48,22 +48,24 @@ def _padded(torch, shape, pad_fill=0.0):
 def _sender(torch, S, kind):
     if kind == "packed":
         return S
-    view = (_token_major(torch, S.shape) if kind == "token-major" else _padded(torch, S.shape))[0]
+    make = _token_major if kind == "token-major" else _padded
+    view = make(torch, S.shape, S.dtype)[0]
     view.copy_(S)
     return view
 
 
-def _receiver(torch, shape, kind):
+def _receiver(torch, shape, kind, dtype=None):
+    dtype = torch.bfloat16 if dtype is None else dtype
     if kind == "packed":
-        return torch.zeros(shape, dtype=torch.bfloat16, device="cuda"), None
+        return torch.zeros(shape, dtype=dtype, device="cuda"), None
     if kind == "token-major":
-        return _token_major(torch, shape)
-    return _padded(torch, shape, pad_fill=7.0)
+        return _token_major(torch, shape, dtype)
+    return _padded(torch, shape, dtype, pad_fill=7.0)
 
 
-def _run(torch, wl, S, R, layer_map, staged):
+def _run(torch, wl, S, R, layer_map, staged, cfg=CFG):
     from paper_2609_32259_amd.path import TransferPath
-    path = TransferPath(wl.seg, S, wl.A, wl.bias, wl.rope, CFG.L_r, CFG.H_r, R=R,
+    path = TransferPath(wl.seg, S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r, R=R,
                         layer_map=layer_map, staged=staged)
     out = path.step()
     torch.cuda.synchronize()
@@ -110,3 +112,25 @@ def test_token_major_against_the_oracle(torch, staged):
     R = _run(torch, wl, S, R, "neighbor3", staged)
     wl_tm = synth.Workload(cfg, wl.seg, S, wl.A, wl.bias, wl.rope)
     Case(cfg, wl_tm, R, tag="gpu-layouts").check_all()
+
+
+def test_fp32_layouts(torch):
+    """The fp32 kernel (any even d_h; here 64) through the same strides."""
+    cfg = synth.TINY_F32.with_(name="fp32 layouts", batch=2)
+    wl = synth.make_workload(cfg, seed=62, device="cuda")
+    T_cap = int(wl.seg.r_len.max()) + 2
+    shape = (wl.seg.batch, cfg.L_r, 2, cfg.H_r, T_cap, cfg.d_h)
+    ref = _run(torch, wl, wl.S, _receiver(torch, shape, "packed", torch.float32)[0], "interp2",
+               False, cfg).clone()
+    for s_kind, r_kind in COMBOS:
+        S = _sender(torch, wl.S, s_kind)
+        R, storage = _receiver(torch, shape, r_kind, torch.float32)
+        print(f"[gpu-layouts] fp32 sender {s_kind} receiver {r_kind} strides S {tuple(S.stride())} "
+              f"R {tuple(R.stride())}", flush=True)
+        got = _run(torch, wl, S, R, "interp2", False, cfg)
+        assert torch.equal(got, ref), (s_kind, r_kind)
+        if r_kind == "padded":
+            assert bool((storage[..., cfg.d_h:] == 7.0).all())
+        if (s_kind, r_kind) == ("token-major", "token-major"):
+            Case(cfg, synth.Workload(cfg, wl.seg, S, wl.A, wl.bias, wl.rope), got,
+                 tag="gpu-layouts").check_all()
