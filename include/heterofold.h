@@ -196,7 +196,10 @@ int32_t hf_build_layer_taps(int32_t L_s, int32_t L_r, int32_t* taps);
  * ptr + b*stride_b + l*stride_l + c*stride_c + h*stride_h + t*stride_t + e
  * (strides in elements; channels contiguous).  The canonical layout
  * [B][L][2][H][T_cap][d_h] is the receiver cache layout [L,2,H_kv,T,d_h] per
- * sequence.  ptr and every stride must keep rows 16-byte aligned.
+ * sequence; any other order of the strides works the same way (token-major
+ * storage [T][H], rows padded past d_h, a cache inside a larger buffer).
+ * ptr and every stride must keep rows 16-byte aligned.  A receiver whose rows
+ * overlap gets racing writes.
  */
 typedef struct hf_kv_desc {
   void* ptr;
