@@ -87,6 +87,33 @@ def test_messy_batched(hf, seed, mode):
     _compare(hf, seg, mode, f"messy seed={seed}")
 
 
+def _random_batch(seed):
+    """A seeded batch of 1-12 sequences mixing the irregular cases: empty and
+    one-character texts, lengths around the 256-row block edge, receiver texts
+    shorter or longer than the sender's, empty sequences, tokens of 1 to 60
+    characters, and empty tokens, gaps and split ends at up to 30% each."""
+    rng = np.random.default_rng(5000 + seed)
+    parts = []
+    for _ in range(int(rng.integers(1, 13))):
+        n_s = int(rng.choice([0, 1, 2, 17, 64, 255, 256, 257, 600]))
+        n_r = int(rng.choice([0, 1, n_s, n_s // 2, n_s + 40, 2 * n_s + 3]))
+        hi_s, hi_r = int(rng.choice([1, 3, 8, 40])), int(rng.choice([1, 4, 9, 60]))
+        sb, se = synth.segment_messy(rng, n_s, 1, hi_s, p_empty=rng.uniform(0, 0.3),
+                                     p_gap=rng.uniform(0, 0.3), p_dup_end=rng.uniform(0, 0.3))
+        rb, re_ = synth.segment_messy(rng, n_r, 1, hi_r, p_empty=rng.uniform(0, 0.3),
+                                      p_gap=rng.uniform(0, 0.3), p_dup_end=rng.uniform(0, 0.3))
+        if len(sb) == 0:  # receiver tokens need sender tokens
+            rb = re_ = np.zeros(0, np.int32)
+        parts.append((sb, se, rb, re_))
+    return synth.concat_segmentations(parts)
+
+
+@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("mode", ["overlap", "ta"])
+def test_random_batches(hf, seed, mode):
+    _compare(hf, _random_batch(seed), mode, f"random seed={seed}")
+
+
 @pytest.mark.parametrize("mode", ["overlap", "ta"])
 def test_long_rows_and_block_edges(hf, mode):
     # Receiver tokens spanning many sender tokens, rows straddling workgroup
