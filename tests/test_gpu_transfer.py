@@ -314,6 +314,42 @@ def test_bf16_batch_of_long_ragged_sequences(torch, staged):
     _compare_full(torch, cfg, synth.Workload(cfg, seg, S, A, bias, rope), "overlap", staged=staged)
 
 
+def _random_case(seed, staged):
+    """A seeded irregular batch: 1-5 sequences of 1-513 sender tokens (around
+    the 64- and 256-row tile edges), receiver tokenizations with empty tokens,
+    gaps and split ends over the same text (sometimes none at all), 3-6 sender
+    and 2-5 receiver layers, 2/4/8 receiver heads (8 on the staged path), per-
+    sequence RoPE offsets and either alignment mode."""
+    rng = np.random.default_rng(7000 + seed)
+    H_r = 8 if staged else int(rng.choice([2, 4, 8]))
+    cfg = synth.LLAMA8B_14B_8K.with_(name=f"random batch {seed}", H_r=H_r,
+                                     L_s=int(rng.integers(3, 7)), L_r=int(rng.integers(2, 6)))
+    parts = []
+    for _ in range(int(rng.integers(1, 6))):
+        n_s = int(rng.choice([1, 7, 63, 64, 65, 255, 256, 300, 513]))
+        sb, se = synth.segment_tokens(rng, n_s, 1, 7)
+        if rng.random() < 0.15:
+            rb = re_ = np.zeros(0, np.int32)
+        else:
+            rb, re_ = synth.segment_messy(rng, int(se[-1]), 1, int(rng.choice([2, 8, 20])),
+                                          p_empty=0.1, p_gap=0.1, p_dup_end=0.1)
+        parts.append((sb, se, rb, re_))
+    seg = synth.concat_segmentations(parts)
+    S = synth.make_cache(cfg, seg, seed=seed, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=seed, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=rng.integers(0, 200, seg.batch).astype(np.int32),
+                             pos0_r=rng.integers(0, 200, seg.batch).astype(np.int32))
+    mode = "overlap" if seed % 2 == 0 else "ta"
+    return cfg, synth.Workload(cfg, seg, S, A, bias, rope), mode
+
+
+@pytest.mark.parametrize("seed", range(6))
+@BOTH_PATHS
+def test_bf16_random_batches(torch, seed, staged):
+    cfg, wl, mode = _random_case(seed, staged)
+    _compare_full(torch, cfg, wl, mode, staged=staged)
+
+
 @BOTH_PATHS
 def test_bf16_rows_past_length_untouched_and_deterministic(torch, staged):
     cfg = synth.LLAMA8B_14B_8K.with_(T_s=260, L_r=4)
