@@ -94,6 +94,43 @@ def test_opts_bf16_key_norm_interpolating(torch, staged):
     _compare(torch, cfg, synth.make_workload(cfg, seed=35, device="cuda"), staged=staged)
 
 
+def _random_paper_case(seed, staged):
+    """A seeded irregular batch through the paper's construction: three-layer
+    map, 1/r and the receiver key norm, sender keys pre- or post-RoPE; 1-4
+    sequences around the tile edges, irregular receiver tokenizations (or
+    none), 3-8 sender and 2-5 receiver layers, 2/4/8 receiver heads (8 on the
+    staged path), per-sequence RoPE offsets, either alignment mode."""
+    rng = np.random.default_rng(8000 + seed)
+    H_r = 8 if staged else (2, 4, 8, 4)[seed]
+    cfg = synth.LLAMA8B_14B_8K.with_(name=f"random paper batch {seed}", H_r=H_r,
+                                     layer_map="neighbor3", paper_opts=True,
+                                     sender_keys_post_rope=bool(seed % 2),
+                                     L_s=int(rng.integers(3, 9)), L_r=int(rng.integers(2, 6)))
+    parts = []
+    for _ in range(int(rng.integers(1, 5))):
+        sb, se = synth.segment_tokens(rng, int(rng.choice([1, 63, 64, 65, 255, 257, 400])), 1, 7)
+        if rng.random() < 0.15:
+            rb = re_ = np.zeros(0, np.int32)
+        else:
+            rb, re_ = synth.segment_messy(rng, int(se[-1]), 1, int(rng.choice([2, 8, 20])),
+                                          p_empty=0.1, p_gap=0.1, p_dup_end=0.1)
+        parts.append((sb, se, rb, re_))
+    seg = synth.concat_segmentations(parts)
+    S = synth.make_cache(cfg, seg, seed=seed, device="cuda")
+    A, bias = synth.make_maps(cfg, seed=seed, device="cuda")
+    rope = synth.rope_params(cfg, pos0_s=rng.integers(0, 200, seg.batch).astype(np.int32),
+                             pos0_r=rng.integers(0, 200, seg.batch).astype(np.int32))
+    wl = synth.Workload(cfg, seg, S, A, bias, rope, synth.make_opts(cfg, seed=seed, device="cuda"))
+    return cfg, wl, ("overlap" if seed < 2 else "ta")
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
+def test_opts_bf16_random_paper_batches(torch, seed, staged):
+    cfg, wl, mode = _random_paper_case(seed, staged)
+    _compare(torch, cfg, wl, mode, staged=staged)
+
+
 @pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
 def test_full_14b_shape_32k_paper_construction(torch, staged):
     """The benchmark's paper-construction workload: every layer and role, on
