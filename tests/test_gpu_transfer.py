@@ -68,6 +68,27 @@ def test_fp32_rope_batched_offsets(torch):
     _compare_full(torch, cfg, wl, "overlap", rope=rope)
 
 
+# Unusual fp32 shapes: head sizes from 4 to 256 channels, 1-6 heads on either
+# side, odd layer counts, RoPE on or off, batches of 1-3 sequences.
+FP32_SHAPES = [(4, 1, 5, 2, 1), (12, 3, 1, 3, 4), (20, 5, 3, 4, 6), (96, 2, 6, 5, 2),
+               (256, 1, 2, 2, 3), (64, 4, 3, 6, 5)]  # d_h, H_s, H_r, L_s, L_r
+
+
+@pytest.mark.parametrize("i", range(len(FP32_SHAPES)))
+def test_fp32_unusual_shapes(torch, i):
+    d_h, H_s, H_r, L_s, L_r = FP32_SHAPES[i]
+    rope = (1.0e4, 5.0e5) if i % 2 == 0 else None
+    cfg = synth.TINY_F32.with_(name=f"fp32 d_h={d_h} {H_s}->{H_r} heads", d_h=d_h, H_s=H_s,
+                               H_r=H_r, L_s=L_s, L_r=L_r, n_chars=500, rope=rope, batch=1 + i % 3)
+    wl = synth.make_workload(cfg, seed=90 + i, device="cuda")
+    if rope is not None:
+        rng = np.random.default_rng(90 + i)
+        wl = synth.Workload(cfg, wl.seg, wl.S, wl.A, wl.bias,
+                            synth.rope_params(cfg, pos0_s=rng.integers(0, 99, cfg.batch),
+                                              pos0_r=rng.integers(0, 99, cfg.batch)))
+    _compare_full(torch, cfg, wl, "overlap" if i < 3 else "ta")
+
+
 # --- bf16, small sizes, every element ----------------------------------------
 
 # The staged path (aligned features written to the workspace, then a separate
