@@ -94,6 +94,36 @@ def test_opts_bf16_key_norm_interpolating(torch, staged):
     _compare(torch, cfg, synth.make_workload(cfg, seed=35, device="cuda"), staged=staged)
 
 
+@pytest.mark.parametrize("staged", [False, True], ids=["fused", "staged"])
+@pytest.mark.parametrize("n_taps", [1, 2])
+def test_opts_bf16_other_tap_counts(torch, n_taps, staged):
+    # The paper's construction with one or two concatenated taps per receiver
+    # layer (explicit tap tables, far-apart and repeated sender layers).
+    from paper_2609_32259_amd.path import TransferPath
+    cfg = synth.LLAMA8B_14B_8K.with_(name=f"14b {n_taps} taps paper", T_s=200, L_r=4,
+                                     layer_map="neighbor3", paper_opts=True,
+                                     sender_keys_post_rope=False)
+    seg = synth.make_segmentation(cfg, seed=36)
+    S = synth.make_cache(cfg, seg, seed=36, device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(36)
+    A = (torch.randn((cfg.L_r, 2, cfg.d_r, n_taps * cfg.d_in), generator=g, device="cuda")
+         / np.sqrt(n_taps * cfg.d_in)).to(torch.bfloat16)
+    _, bias = synth.make_maps(cfg, seed=36, device="cuda")
+    taps = np.array([[0, 31, 7][:n_taps], [5, 5, 5][:n_taps], [31, 0, 16][:n_taps],
+                     [12, 13, 14][:n_taps]], np.int32)
+    wl = synth.Workload(cfg, seg, S, A, bias, synth.rope_params(cfg),
+                        synth.make_opts(cfg, seed=36, device="cuda"))
+    print(f"[gpu-opts] {cfg.name} T_r={list(wl.seg.r_len)} staged={staged}", flush=True)
+    path = TransferPath(wl.seg, wl.S, wl.A, wl.bias, wl.rope, cfg.L_r, cfg.H_r,
+                        layer_map="neighbor3", opts=wl.opts, staged=staged)
+    path.build_alignment()
+    path.layer_map = taps
+    path.transfer()
+    torch.cuda.synchronize()
+    Case(cfg, wl, path.R, "overlap", layer_map=taps, tag="gpu-opts",
+         scale_product=path.staged).check_all()
+
+
 def _random_paper_case(seed, staged):
     """A seeded irregular batch through the paper's construction: three-layer
     map, 1/r and the receiver key norm, sender keys pre- or post-RoPE; 1-4
